@@ -1,0 +1,614 @@
+// libjf C ABI: validation, buffer layout, weight packing and the launch
+// sequence of one Jacobi iteration (see include/jf.h for the contract).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/jf.h"
+#include "jf_internal.h"
+
+using namespace jf;
+
+// ---- errors ------------------------------------------------------------------------
+static thread_local std::string g_err;
+
+static jf_status fail(jf_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return fail(JF_E_HIP, "%s: %s (%s:%d)", #expr, hipGetErrorString(e_), __FILE__, __LINE__); \
+  } while (0)
+
+extern "C" const char* jf_last_error(void) { return g_err.c_str(); }
+
+// ---- layout ------------------------------------------------------------------------
+namespace {
+
+constexpr int kMaxSplits = 32;
+
+size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+struct Layout {
+  // element counts / byte offsets
+  size_t esz;                      // element size of cfg.dtype
+  int Rp;                          // max_rows rounded up to 16
+  int qkv_rows;                    // (H + 2G) * hd
+  int n_pages;                     // pages per layer
+  // packed (bytes)
+  size_t l_qkv, l_o, l_gu, l_down, l_an, l_fn, layer_bytes;
+  size_t p_lm, p_final, p_embed, packed_bytes;
+  // kv (bytes)
+  size_t page_bytes, kv_layer_bytes, kv_bytes;
+  // workspace (bytes)
+  size_t w_state, w_h, w_xn, w_q, w_attn, w_act, w_opart, w_ml, w_lm, w_g, w_parent, w_pos,
+      w_vis, w_cos, w_sin, w_pt, w_rowmap, w_result, ws_bytes;
+};
+
+jf_status check_config(const jf_config* c) {
+  if (!c) return fail(JF_E_INVAL, "config is null");
+  if (c->dtype != JF_F32 && c->dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", c->dtype);
+  if (c->n_layers < 1 || c->d_model < 128 || c->n_heads < 1 || c->n_kv_heads < 1 || c->d_ffn < 128 ||
+      c->vocab < 16)
+    return fail(JF_E_SHAPE, "non-positive or too small dimension");
+  if (c->d_model % 128 || c->d_ffn % 128) return fail(JF_E_SHAPE, "d_model and d_ffn must be multiples of 128");
+  if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
+    return fail(JF_E_SHAPE, "head_dim must be 32, 64 or 128");
+  if (c->n_heads % c->n_kv_heads) return fail(JF_E_SHAPE, "n_heads must be a multiple of n_kv_heads");
+  if ((c->n_heads * c->head_dim) % 128) return fail(JF_E_SHAPE, "n_heads * head_dim must be a multiple of 128");
+  if (c->vocab % 16) return fail(JF_E_SHAPE, "vocab must be a multiple of 16");
+  if (c->max_rows < 1 || c->max_rows > 256) return fail(JF_E_SHAPE, "max_rows must be in [1, 256]");
+  if (c->max_ctx < 64 || c->max_ctx % 64) return fail(JF_E_SHAPE, "max_ctx must be a positive multiple of 64");
+  if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return fail(JF_E_INVAL, "rms_eps / rope_base out of range");
+  return JF_OK;
+}
+
+Layout make_layout(const jf_config& c) {
+  Layout L{};
+  L.esz = c.dtype == JF_BF16 ? 2 : 4;
+  L.Rp = (c.max_rows + 15) / 16 * 16;
+  const size_t d = c.d_model, F = c.d_ffn, V = c.vocab, Hhd = (size_t)c.n_heads * c.head_dim;
+  L.qkv_rows = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+  L.n_pages = c.max_ctx / kPage;
+  size_t off = 0;
+  L.l_qkv = off; off = align_up(off + (size_t)L.qkv_rows * d * L.esz);
+  L.l_o = off; off = align_up(off + d * Hhd * L.esz);
+  L.l_gu = off; off = align_up(off + 2 * F * d * L.esz);
+  L.l_down = off; off = align_up(off + d * F * L.esz);
+  L.l_an = off; off = align_up(off + d * 4);
+  L.l_fn = off; off = align_up(off + d * 4);
+  L.layer_bytes = off;
+  off = L.layer_bytes * c.n_layers;
+  L.p_lm = off; off = align_up(off + V * d * L.esz);
+  L.p_final = off; off = align_up(off + d * 4);
+  L.p_embed = off; off = align_up(off + V * d * L.esz);
+  L.packed_bytes = off;
+
+  L.page_bytes = (size_t)2 * c.n_kv_heads * kPage * c.head_dim * L.esz;
+  L.kv_layer_bytes = L.page_bytes * L.n_pages;
+  L.kv_bytes = L.kv_layer_bytes * c.n_layers;
+
+  const size_t Rp = L.Rp;
+  off = 0;
+  L.w_state = off; off = align_up(off + 64);
+  L.w_h = off; off = align_up(off + Rp * d * 4);
+  L.w_xn = off; off = align_up(off + Rp * d * L.esz);
+  L.w_q = off; off = align_up(off + Rp * Hhd * L.esz);
+  L.w_attn = off; off = align_up(off + Rp * Hhd * L.esz);
+  L.w_act = off; off = align_up(off + Rp * F * L.esz);
+  L.w_opart = off; off = align_up(off + (size_t)kMaxSplits * Rp * c.n_heads * c.head_dim * 4);
+  L.w_ml = off; off = align_up(off + (size_t)kMaxSplits * Rp * c.n_heads * 2 * 4);
+  L.w_lm = off; off = align_up(off + (V / 16) * Rp * 8);
+  L.w_g = off; off = align_up(off + Rp * 4);
+  L.w_parent = off; off = align_up(off + Rp * 4);
+  L.w_pos = off; off = align_up(off + Rp * 4);
+  L.w_vis = off; off = align_up(off + Rp * 4 * 8);
+  L.w_cos = off; off = align_up(off + (size_t)c.max_ctx * (c.head_dim / 2) * 4);
+  L.w_sin = off; off = align_up(off + (size_t)c.max_ctx * (c.head_dim / 2) * 4);
+  L.w_pt = off; off = align_up(off + (size_t)L.n_pages * 4);
+  size_t maxrows = std::max<size_t>({(size_t)L.qkv_rows, 2 * F, d, V});
+  L.w_rowmap = off; off = align_up(off + maxrows * 4);
+  L.w_result = off; off = align_up(off + 64);
+  L.ws_bytes = off;
+  return L;
+}
+
+}  // namespace
+
+struct jf_model {
+  jf_config cfg;
+  Layout L;
+  char* packed;
+  char* kv;
+  char* ws;
+  int C_ub;          // host upper bound of the committed length
+  int last_rows;     // rows of the last step (0: no step to commit)
+  int last_tree;     // last step was a multi-block step
+  int32_t* state() { return reinterpret_cast<int32_t*>(ws + L.w_state); }
+  int32_t* flags() { return state() + 1; }
+  template <typename P> P* at(size_t off) { return reinterpret_cast<P*>(ws + off); }
+  char* layer(int l) { return packed + (size_t)l * L.layer_bytes; }
+  char* kv_layer(int l) { return kv + (size_t)l * L.kv_layer_bytes; }
+};
+
+extern "C" jf_status jf_query_sizes(const jf_config* cfg, size_t* packed_bytes, size_t* kv_bytes,
+                                    size_t* ws_bytes) {
+  jf_status s = check_config(cfg);
+  if (s != JF_OK) return s;
+  if (!packed_bytes || !kv_bytes || !ws_bytes) return fail(JF_E_INVAL, "null output pointer");
+  Layout L = make_layout(*cfg);
+  *packed_bytes = L.packed_bytes;
+  *kv_bytes = L.kv_bytes;
+  *ws_bytes = L.ws_bytes;
+  return JF_OK;
+}
+
+// Row order of the fused QKV matrix: q heads, k heads, v heads; inside every
+// 16-row tile of a q/k head, rows 0..7 are dims 8t..8t+7 and rows 8..15 are
+// dims hd/2+8t..hd/2+8t+7 so each RoPE pair (i, i + hd/2) sits in one tile.
+static std::vector<int32_t> qkv_rowmap(const jf_config& c) {
+  std::vector<int32_t> m;
+  const int hd = c.head_dim, half = hd / 2;
+  auto add_head = [&](int src, int head, bool rope) {
+    for (int w = 0; w < hd; ++w) {
+      int dim = w;
+      if (rope) {
+        int t = w / 16, cc = w % 16;
+        dim = cc < 8 ? 8 * t + cc : half + 8 * t + (cc - 8);
+      }
+      m.push_back((src << 24) | (head * hd + dim));
+    }
+  };
+  for (int h = 0; h < c.n_heads; ++h) add_head(0, h, true);
+  for (int h = 0; h < c.n_kv_heads; ++h) add_head(1, h, true);
+  for (int h = 0; h < c.n_kv_heads; ++h) add_head(2, h, false);
+  return m;
+}
+
+// gate/up interleaved by 16-row tiles: tile 2t = gate rows 16t.., 2t+1 = up rows 16t..
+static std::vector<int32_t> gateup_rowmap(const jf_config& c) {
+  std::vector<int32_t> m;
+  for (int t = 0; t < c.d_ffn / 16; ++t) {
+    for (int i = 0; i < 16; ++i) m.push_back((0 << 24) | (16 * t + i));
+    for (int i = 0; i < 16; ++i) m.push_back((1 << 24) | (16 * t + i));
+  }
+  return m;
+}
+
+extern "C" jf_status jf_model_load(const jf_config* cfg, const void* const* d_weights,
+                                   int32_t n_weights, void* d_packed, void* d_kv, void* d_ws,
+                                   jf_stream stream, jf_model** out) {
+  jf_status s = check_config(cfg);
+  if (s != JF_OK) return s;
+  if (!d_weights || !d_packed || !d_kv || !d_ws || !out) return fail(JF_E_INVAL, "null pointer argument");
+  if (n_weights != 3 + 9 * cfg->n_layers)
+    return fail(JF_E_INVAL, "n_weights = %d, expected %d", n_weights, 3 + 9 * cfg->n_layers);
+  for (int i = 0; i < n_weights; ++i)
+    if (!d_weights[i]) return fail(JF_E_INVAL, "weight %d is null", i);
+  *out = nullptr;
+  hipStream_t st = (hipStream_t)stream;
+  jf_model* m = new (std::nothrow) jf_model();
+  if (!m) return fail(JF_E_INVAL, "out of host memory");
+  m->cfg = *cfg;
+  m->L = make_layout(*cfg);
+  m->packed = (char*)d_packed;
+  m->kv = (char*)d_kv;
+  m->ws = (char*)d_ws;
+  const jf_config& c = *cfg;
+  const Layout& L = m->L;
+  const int dt = c.dtype;
+  const int d = c.d_model, F = c.d_ffn, V = c.vocab, Hhd = c.n_heads * c.head_dim;
+
+  auto bail = [&](jf_status st_) { delete m; return st_; };
+#define LOAD_TRY(expr)                                                                      \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return bail(fail(JF_E_HIP, "%s: %s", #expr, hipGetErrorString(e_)));                 \
+  } while (0)
+
+  // Host tables: rope cos/sin (float64 math, rounded to float32), page table.
+  const int half = c.head_dim / 2;
+  std::vector<float> cs((size_t)c.max_ctx * half), sn((size_t)c.max_ctx * half);
+  for (int p = 0; p < c.max_ctx; ++p)
+    for (int i = 0; i < half; ++i) {
+      double inv = std::pow((double)c.rope_base, -(2.0 * i) / c.head_dim);
+      double ang = (double)p * inv;
+      cs[(size_t)p * half + i] = (float)std::cos(ang);
+      sn[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  std::vector<int32_t> pt(L.n_pages);
+  for (int i = 0; i < L.n_pages; ++i) pt[i] = i;
+  std::vector<int32_t> rm_qkv = qkv_rowmap(c), rm_gu = gateup_rowmap(c);
+
+  LOAD_TRY(hipMemsetAsync(d_kv, 0, L.kv_bytes, st));
+  LOAD_TRY(hipMemsetAsync(m->ws + L.w_state, 0, 64, st));
+  LOAD_TRY(hipMemcpyAsync(m->ws + L.w_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, st));
+  LOAD_TRY(hipMemcpyAsync(m->ws + L.w_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, st));
+  LOAD_TRY(hipMemcpyAsync(m->ws + L.w_pt, pt.data(), pt.size() * 4, hipMemcpyHostToDevice, st));
+
+  int32_t* rowmap = m->at<int32_t>(L.w_rowmap);
+  const size_t esz = L.esz;
+  // embedding (natural layout) and the LM head / final norm
+  LOAD_TRY(hipMemcpyAsync(m->packed + L.p_embed, d_weights[0], (size_t)V * d * esz,
+                          hipMemcpyDeviceToDevice, st));
+  const int base_final = 1 + 9 * c.n_layers;
+  LOAD_TRY(launch_to_f32(dt, d_weights[base_final], (float*)(m->packed + L.p_final), d, st));
+  {
+    const void* src[1] = {d_weights[base_final + 1]};
+    LOAD_TRY(launch_pack(dt, V, d, src, 1, nullptr, m->packed + L.p_lm, st));
+  }
+  for (int l = 0; l < c.n_layers; ++l) {
+    const void* const* w = d_weights + 1 + 9 * l;
+    char* lp = m->layer(l);
+    LOAD_TRY(launch_to_f32(dt, w[0], (float*)(lp + L.l_an), d, st));
+    LOAD_TRY(launch_to_f32(dt, w[5], (float*)(lp + L.l_fn), d, st));
+    LOAD_TRY(hipMemcpyAsync(rowmap, rm_qkv.data(), rm_qkv.size() * 4, hipMemcpyHostToDevice, st));
+    const void* qkv[3] = {w[1], w[2], w[3]};
+    LOAD_TRY(launch_pack(dt, L.qkv_rows, d, qkv, 3, rowmap, lp + L.l_qkv, st));
+    const void* o[1] = {w[4]};
+    LOAD_TRY(launch_pack(dt, d, Hhd, o, 1, nullptr, lp + L.l_o, st));
+    LOAD_TRY(hipStreamSynchronize(st));  // rowmap reused below
+    LOAD_TRY(hipMemcpyAsync(rowmap, rm_gu.data(), rm_gu.size() * 4, hipMemcpyHostToDevice, st));
+    const void* gu[2] = {w[6], w[7]};
+    LOAD_TRY(launch_pack(dt, 2 * F, d, gu, 2, rowmap, lp + L.l_gu, st));
+    const void* dn[1] = {w[8]};
+    LOAD_TRY(launch_pack(dt, d, F, dn, 1, nullptr, lp + L.l_down, st));
+    LOAD_TRY(hipStreamSynchronize(st));
+  }
+  LOAD_TRY(hipStreamSynchronize(st));
+#undef LOAD_TRY
+  m->C_ub = 0;
+  m->last_rows = 0;
+  m->last_tree = 0;
+  *out = m;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_model_free(jf_model* m) {
+  if (!m) return fail(JF_E_INVAL, "model is null");
+  delete m;
+  return JF_OK;
+}
+
+// ---- forward pass of one step ---------------------------------------------------------
+// Runs rows through all layers; the K/V of row r land in cache slot C + r.
+// lm: 0 = no LM head, 1 = all rows, 2 = last row only.  g receives the argmax.
+static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegArgs& sg, int lm,
+                         int32_t* d_g, float* d_logits, hipStream_t st) {
+  const jf_config& c = m->cfg;
+  const Layout& L = m->L;
+  const int dt = c.dtype;
+  const int d = c.d_model, F = c.d_ffn, H = c.n_heads, G = c.n_kv_heads, hd = c.head_dim;
+  const int Hhd = H * hd;
+  int32_t* state = m->state();
+  float* h = m->at<float>(L.w_h);
+  void* xn = m->ws + L.w_xn;
+  int32_t* pos = m->at<int32_t>(L.w_pos);
+
+  HIP_TRY(launch_tree(sg, R, state, m->flags(), m->at<int32_t>(L.w_parent), pos,
+                      m->at<uint64_t>(L.w_vis), st));
+  HIP_TRY(launch_embed_norm(dt, d_tokens, R, m->packed + L.p_embed, (const float*)(m->layer(0) + L.l_an),
+                            d, c.vocab, c.rms_eps, h, xn, m->flags(), st));
+  const int splits = attn_splits(std::min(m->C_ub + R, c.max_ctx));
+  for (int l = 0; l < c.n_layers; ++l) {
+    char* lp = m->layer(l);
+    // a3: QKV + RoPE + K/V into the cache slots C + r
+    {
+      GemmShape gs{R, m->L.qkv_rows, d, 1, 1};
+      gemm_plan(gs, EPI_QKV);
+      Epi ep{};
+      ep.kind = EPI_QKV; ep.R = R;
+      ep.q = m->ws + L.w_q; ep.kv = m->kv_layer(l); ep.page_table = m->at<int32_t>(L.w_pt);
+      ep.pos = pos; ep.state = state; ep.rope_cos = m->at<float>(L.w_cos); ep.rope_sin = m->at<float>(L.w_sin);
+      ep.H = H; ep.G = G; ep.hd = hd; ep.max_ctx = c.max_ctx; ep.flags = m->flags();
+      HIP_TRY(launch_gemm(dt, xn, d, lp + L.l_qkv, gs, ep, st));
+    }
+    // a4: attention
+    {
+      AttnArgs a{};
+      a.H = H; a.G = G; a.hd = hd; a.R = R; a.max_ctx = c.max_ctx; a.splits = splits;
+      a.q = m->ws + L.w_q; a.kv = m->kv_layer(l); a.page_table = m->at<int32_t>(L.w_pt);
+      a.state = state; a.vis = m->at<uint64_t>(L.w_vis);
+      a.o_part = m->at<float>(L.w_opart); a.ml_part = m->at<float>(L.w_ml); a.out = m->ws + L.w_attn;
+      HIP_TRY(launch_attention(dt, a, st));
+    }
+    // a5: O projection + residual
+    {
+      GemmShape gs{R, d, Hhd, 1, 1};
+      gemm_plan(gs, EPI_RESID);
+      Epi ep{};
+      ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
+      HIP_TRY(launch_gemm(dt, m->ws + L.w_attn, Hhd, lp + L.l_o, gs, ep, st));
+    }
+    // a6: RMSNorm, gate/up + SwiGLU, down + residual
+    HIP_TRY(launch_rmsnorm(dt, h, d, R, (const float*)(lp + L.l_fn), d, c.rms_eps, xn, d, st));
+    {
+      GemmShape gs{R, 2 * F, d, 2, 1};
+      gemm_plan(gs, EPI_SWIGLU);
+      Epi ep{};
+      ep.kind = EPI_SWIGLU; ep.R = R; ep.act = m->ws + L.w_act; ep.lda = F;
+      HIP_TRY(launch_gemm(dt, xn, d, lp + L.l_gu, gs, ep, st));
+    }
+    {
+      GemmShape gs{R, d, F, 1, 1};
+      gemm_plan(gs, EPI_RESID);
+      Epi ep{};
+      ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
+      HIP_TRY(launch_gemm(dt, m->ws + L.w_act, F, lp + L.l_down, gs, ep, st));
+    }
+    const float* next_gain = l + 1 < c.n_layers ? (const float*)(m->layer(l + 1) + L.l_an)
+                                                : (const float*)(m->packed + L.p_final);
+    if (l + 1 < c.n_layers || lm != 0)
+      HIP_TRY(launch_rmsnorm(dt, h, d, R, next_gain, d, c.rms_eps, xn, d, st));
+  }
+  if (lm == 0) return JF_OK;
+  // a7: LM head with fused argmax (logits optional)
+  const int Rl = lm == 2 ? 1 : R;
+  const void* X = lm == 2 ? (const void*)(m->ws + L.w_xn + (size_t)(R - 1) * d * L.esz) : xn;
+  GemmShape gs{Rl, c.vocab, d, 1, 1};
+  gemm_plan(gs, EPI_ARGMAX);
+  Epi ep{};
+  ep.kind = EPI_ARGMAX; ep.R = Rl; ep.part = m->at<uint64_t>(L.w_lm); ep.part_stride = L.Rp;
+  ep.logits = d_logits; ep.ldl = c.vocab;
+  HIP_TRY(launch_gemm(dt, X, d, m->packed + L.p_lm, gs, ep, st));
+  HIP_TRY(launch_argmax_reduce(ep.part, (int)gemm_blocks(gs), L.Rp, Rl, d_g, st));
+  return JF_OK;
+}
+
+// Capacity check against the host's upper bound of C.  The bound only grows
+// by the rows of each committed step (the accepted count stays on the
+// device); when it would exceed max_ctx the exact C is read back (one stream
+// synchronisation) before refusing.
+static jf_status check_rows(jf_model* m, int R, hipStream_t st) {
+  if (R < 1 || R > m->cfg.max_rows)
+    return fail(JF_E_CAPACITY, "rows %d outside [1, max_rows=%d]", R, m->cfg.max_rows);
+  if (m->C_ub + R > m->cfg.max_ctx) {
+    int32_t v = 0;
+    HIP_TRY(hipMemcpyAsync(&v, m->state(), 4, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    m->C_ub = v;
+  }
+  if (m->C_ub + R > m->cfg.max_ctx)
+    return fail(JF_E_CAPACITY, "committed length %d + rows %d exceeds max_ctx %d", m->C_ub, R,
+                m->cfg.max_ctx);
+  return JF_OK;
+}
+
+extern "C" jf_status jf_prefill(jf_model* m, const int32_t* d_tokens, int32_t n, int32_t* d_pending,
+                                jf_stream stream) {
+  if (!m || !d_tokens || !d_pending) return fail(JF_E_INVAL, "null pointer argument");
+  if (m->C_ub != 0) return fail(JF_E_STATE, "prefill needs an empty cache (truncate to 0 first)");
+  if (n < 1 || n > m->cfg.max_ctx) return fail(JF_E_CAPACITY, "prompt length %d outside [1, max_ctx]", n);
+  hipStream_t st = (hipStream_t)stream;
+  const int chunk = m->cfg.max_rows;
+  for (int s = 0; s < n; s += chunk) {
+    const int R = std::min(chunk, n - s);
+    SegArgs sg{};
+    sg.n = 1; sg.first[0] = 0; sg.nrows[0] = R; sg.attach[0] = -1; sg.role[0] = 0; sg.verify_from[0] = 1;
+    const bool last = s + R == n;
+    jf_status r = forward(m, d_tokens + s, R, sg, last ? 2 : 0, d_pending, nullptr, st);
+    if (r != JF_OK) return r;
+    HIP_TRY(launch_commit(m->cfg.dtype, m->kv, m->cfg.n_layers, m->L.n_pages, m->cfg.n_kv_heads,
+                          m->cfg.head_dim, m->at<int32_t>(m->L.w_pt), m->state(), nullptr,
+                          m->at<int32_t>(m->L.w_result), 0, R, m->cfg.max_ctx, st));
+    m->C_ub += R;
+  }
+  m->last_rows = 0;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_jacobi_step(jf_model* m, const int32_t* d_draft, int32_t n, int32_t mode,
+                                    uint64_t pad_seed, int32_t* d_argmax, jf_step_result* d_result,
+                                    int32_t* d_next_draft, float* d_logits, jf_stream stream) {
+  if (!m || !d_draft || !d_argmax || !d_result || !d_next_draft)
+    return fail(JF_E_INVAL, "null pointer argument");
+  if (mode != 0 && mode != 1) return fail(JF_E_INVAL, "mode must be 0 (block) or 1 (window)");
+  if (m->C_ub == 0) return fail(JF_E_STATE, "empty cache: prefill the prompt first");
+  hipStream_t st = (hipStream_t)stream;
+  jf_status s = check_rows(m, n, st);
+  if (s != JF_OK) return s;
+  SegArgs sg{};
+  sg.n = 1; sg.first[0] = 0; sg.nrows[0] = n; sg.attach[0] = -1; sg.role[0] = 0; sg.verify_from[0] = 1;
+  s = forward(m, d_draft, n, sg, 1, d_argmax, d_logits, st);
+  if (s != JF_OK) return s;
+  HIP_TRY(launch_accept_linear(d_draft, d_argmax, n, mode, pad_seed, m->cfg.vocab, m->state(),
+                               m->flags(), reinterpret_cast<int32_t*>(d_result), d_next_draft, st));
+  m->last_rows = n;
+  m->last_tree = 0;
+  return JF_OK;
+}
+
+static jf_status check_segments(const jf_segment* segs, int n_segs, int R, SegArgs* out) {
+  if (!segs) return fail(JF_E_INVAL, "segments are null");
+  if (n_segs < 1 || n_segs > JF_MAX_SEGMENTS)
+    return fail(JF_E_INVAL, "n_segs %d outside [1, %d]", n_segs, JF_MAX_SEGMENTS);
+  int next = 0;
+  for (int i = 0; i < n_segs; ++i) {
+    const jf_segment& s = segs[i];
+    if (s.first_row != next || s.n_rows < 1)
+      return fail(JF_E_INVAL, "segment %d does not continue the row order", i);
+    if (s.attach_row < -1 || s.attach_row >= s.first_row)
+      return fail(JF_E_INVAL, "segment %d must attach to an earlier row or -1", i);
+    if (s.role < JF_ROLE_RA || s.role > JF_ROLE_PSEUDO)
+      return fail(JF_E_INVAL, "segment %d has an unknown role", i);
+    if (s.verify_from < 0 || s.verify_from > s.n_rows)
+      return fail(JF_E_INVAL, "segment %d verify_from outside [0, n_rows]", i);
+    if (i > 0 && s.role == JF_ROLE_RA) return fail(JF_E_INVAL, "only segment 0 may be real-active");
+    next += s.n_rows;
+    out->first[i] = s.first_row; out->nrows[i] = s.n_rows; out->attach[i] = s.attach_row;
+    out->role[i] = s.role; out->verify_from[i] = s.verify_from;
+  }
+  if (next != R) return fail(JF_E_INVAL, "segments cover %d rows, R = %d", next, R);
+  if (segs[0].attach_row != -1 || segs[0].role != JF_ROLE_RA || segs[0].verify_from != 1)
+    return fail(JF_E_INVAL, "segment 0 must be the real-active draft (attach -1, verify_from 1)");
+  out->n = n_segs;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_multiblock_step(jf_model* m, const int32_t* d_tokens, int32_t R,
+                                        const jf_segment* segs, int32_t n_segs, int32_t* d_argmax,
+                                        int32_t* d_seg_accept, jf_step_result* d_result,
+                                        int32_t* d_path, float* d_logits, jf_stream stream) {
+  if (!m || !d_tokens || !d_argmax || !d_seg_accept || !d_result || !d_path)
+    return fail(JF_E_INVAL, "null pointer argument");
+  if (m->C_ub == 0) return fail(JF_E_STATE, "empty cache: prefill the prompt first");
+  hipStream_t st = (hipStream_t)stream;
+  SegArgs sg{};
+  jf_status s = check_segments(segs, n_segs, R, &sg);
+  if (s != JF_OK) return s;
+  s = check_rows(m, R, st);
+  if (s != JF_OK) return s;
+  s = forward(m, d_tokens, R, sg, 1, d_argmax, d_logits, st);
+  if (s != JF_OK) return s;
+  HIP_TRY(launch_accept_tree(sg, d_tokens, d_argmax, m->at<int32_t>(m->L.w_parent), R, m->flags(),
+                             d_seg_accept, reinterpret_cast<int32_t*>(d_result), d_path, st));
+  m->last_rows = R;
+  m->last_tree = 1;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_commit_kv(jf_model* m, const int32_t* d_path, const jf_step_result* d_result,
+                                  int32_t max_commit, jf_stream stream) {
+  if (!m || !d_result) return fail(JF_E_INVAL, "null pointer argument");
+  if (m->last_rows == 0) return fail(JF_E_STATE, "no step to commit");
+  if (m->last_tree && !d_path) return fail(JF_E_INVAL, "a multi-block step needs its path");
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(launch_commit(m->cfg.dtype, m->kv, m->cfg.n_layers, m->L.n_pages, m->cfg.n_kv_heads,
+                        m->cfg.head_dim, m->at<int32_t>(m->L.w_pt), m->state(), d_path,
+                        reinterpret_cast<const int32_t*>(d_result), max_commit, 0, m->cfg.max_ctx, st));
+  int add = m->last_rows;
+  if (max_commit > 0 && max_commit < add) add = max_commit;
+  m->C_ub = std::min(m->C_ub + add, m->cfg.max_ctx);
+  m->last_rows = 0;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_kv_length(jf_model* m, int32_t* out, jf_stream stream) {
+  if (!m || !out) return fail(JF_E_INVAL, "null pointer argument");
+  hipStream_t st = (hipStream_t)stream;
+  int32_t v = 0;
+  HIP_TRY(hipMemcpyAsync(&v, m->state(), 4, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  *out = v;
+  m->C_ub = v;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_kv_truncate(jf_model* m, int32_t new_len, jf_stream stream) {
+  if (!m) return fail(JF_E_INVAL, "model is null");
+  int32_t C = 0;
+  jf_status s = jf_kv_length(m, &C, stream);
+  if (s != JF_OK) return s;
+  if (new_len < 0 || new_len > C) return fail(JF_E_STATE, "truncate to %d, committed length is %d", new_len, C);
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(launch_set_int(m->state(), new_len, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  m->C_ub = new_len;
+  m->last_rows = 0;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_kv_set_page_table(jf_model* m, const int32_t* h_table, int32_t n, jf_stream stream) {
+  if (!m || !h_table) return fail(JF_E_INVAL, "null pointer argument");
+  if (n != m->L.n_pages) return fail(JF_E_INVAL, "page table needs %d entries, got %d", m->L.n_pages, n);
+  std::vector<char> seen(n, 0);
+  for (int i = 0; i < n; ++i) {
+    if (h_table[i] < 0 || h_table[i] >= n || seen[h_table[i]])
+      return fail(JF_E_INVAL, "page table entry %d is out of range or repeated", i);
+    seen[h_table[i]] = 1;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(hipMemcpyAsync(m->ws + m->L.w_pt, h_table, (size_t)n * 4, hipMemcpyHostToDevice, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  return JF_OK;
+}
+
+// ---- component calls ---------------------------------------------------------------------
+extern "C" size_t jf_attention_ws_bytes(int32_t n_heads, int32_t head_dim, int32_t R) {
+  if (n_heads < 1 || head_dim < 1 || R < 1) return 0;
+  return (size_t)kMaxSplits * R * n_heads * (head_dim + 2) * 4 + 256;
+}
+
+extern "C" jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, int32_t dtype,
+                                  int32_t C, int32_t R, const void* d_q, const void* d_kv_layer,
+                                  const int32_t* d_page_table, const uint64_t* d_vis, void* d_out,
+                                  void* d_ws, jf_stream stream) {
+  if (!d_q || !d_kv_layer || !d_page_table || !d_out || !d_ws) return fail(JF_E_INVAL, "null pointer argument");
+  if (dtype != JF_F32 && dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", dtype);
+  if (n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads) return fail(JF_E_SHAPE, "bad head counts");
+  if (head_dim != 32 && head_dim != 64 && head_dim != 128) return fail(JF_E_SHAPE, "head_dim must be 32, 64 or 128");
+  if (R < 1 || R > 256 || C < 0) return fail(JF_E_CAPACITY, "R must be in [1, 256] and C >= 0");
+  AttnArgs a{};
+  a.H = n_heads; a.G = n_kv_heads; a.hd = head_dim; a.R = R; a.max_ctx = C + R;
+  a.splits = attn_splits(C + R);
+  a.q = d_q; a.kv = d_kv_layer; a.page_table = d_page_table; a.state = nullptr; a.C_host = C;
+  a.vis = d_vis;
+  a.o_part = (float*)d_ws;
+  a.ml_part = (float*)((char*)d_ws + (size_t)kMaxSplits * R * n_heads * head_dim * 4);
+  a.out = d_out;
+  HIP_TRY(launch_attention(dtype, a, (hipStream_t)stream));
+  return JF_OK;
+}
+
+extern "C" size_t jf_packed_matrix_bytes(int32_t rows, int32_t cols, int32_t dtype) {
+  if (rows < 1 || cols < 1) return 0;
+  return (size_t)rows * cols * (dtype == JF_BF16 ? 2 : 4);
+}
+
+extern "C" jf_status jf_pack_matrix(int32_t rows, int32_t cols, int32_t dtype, const void* d_src,
+                                    void* d_packed, jf_stream stream) {
+  if (!d_src || !d_packed) return fail(JF_E_INVAL, "null pointer argument");
+  if (dtype != JF_F32 && dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", dtype);
+  if (rows < 16 || rows % 16 || cols < 128 || cols % 128)
+    return fail(JF_E_SHAPE, "rows must be a multiple of 16 and cols of 128");
+  const void* src[1] = {d_src};
+  HIP_TRY(launch_pack(dtype, rows, cols, src, 1, nullptr, d_packed, (hipStream_t)stream));
+  return JF_OK;
+}
+
+extern "C" size_t jf_lm_head_ws_bytes(int32_t R, int32_t V) {
+  if (R < 1 || V < 16) return 0;
+  return (size_t)(V / 16) * R * 8 + 256;
+}
+
+extern "C" jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t dtype, const void* d_x,
+                                       const void* d_w_packed, const int32_t* d_draft, int32_t* d_argmax,
+                                       jf_step_result* d_result, float* d_logits, void* d_ws,
+                                       jf_stream stream) {
+  if (!d_x || !d_w_packed || !d_argmax || !d_ws) return fail(JF_E_INVAL, "null pointer argument");
+  if (d_draft && !d_result) return fail(JF_E_INVAL, "acceptance needs d_result");
+  if (dtype != JF_F32 && dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", dtype);
+  if (R < 1 || R > 256) return fail(JF_E_CAPACITY, "R must be in [1, 256]");
+  if (d < 128 || d % 128 || V < 16 || V % 16) return fail(JF_E_SHAPE, "d multiple of 128, V multiple of 16");
+  hipStream_t st = (hipStream_t)stream;
+  GemmShape gs{R, V, d, 1, 1};
+  gemm_plan(gs, EPI_ARGMAX);
+  Epi ep{};
+  ep.kind = EPI_ARGMAX; ep.R = R; ep.part = (uint64_t*)d_ws; ep.part_stride = R;
+  ep.logits = d_logits; ep.ldl = V;
+  HIP_TRY(launch_gemm(dtype, d_x, d, d_w_packed, gs, ep, st));
+  HIP_TRY(launch_argmax_reduce(ep.part, (int)gemm_blocks(gs), R, R, d_argmax, st));
+  if (d_draft) {
+    int32_t* zero = (int32_t*)((char*)d_ws + (size_t)(V / 16) * R * 8);
+    HIP_TRY(launch_set_int(zero, 0, st));
+    HIP_TRY(launch_accept_linear(d_draft, d_argmax, R, 0, 0, V, zero, nullptr,
+                                 reinterpret_cast<int32_t*>(d_result), nullptr, st));
+  }
+  return JF_OK;
+}

@@ -1,0 +1,127 @@
+// Device-side building blocks for gfx950 (CDNA4): element types, bf16
+// rounding, MFMA fragments and the packed-weight layout shared by the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace jf {
+
+typedef uint16_t bf16_t;  // bf16 storage (bit pattern)
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// ---- scalar conversions -----------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+// Round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16_t>(bf16_t v) { return bf16_to_f32(v); }
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
+
+// ---- MFMA fragments: 8 consecutive K-elements per lane ------------------------
+// A 16x16 MFMA tile is built from lane l holding row/column (l % 16) and the
+// K-group (l / 16).  Any fixed assignment of K indices to (group, element)
+// gives the same contraction as long as both operands use it, which lets
+// every lane load 8 (or 32) contiguous elements.
+template <typename T> struct Frag;
+template <> struct Frag<bf16_t> { uint4 v; };           // 8 x bf16 (16 B)
+template <> struct Frag<float> { float4 lo, hi; };      // 8 x f32  (32 B)
+
+template <typename T> __device__ __forceinline__ Frag<T> frag_zero();
+template <> __device__ __forceinline__ Frag<bf16_t> frag_zero<bf16_t>() {
+  Frag<bf16_t> f; f.v = make_uint4(0, 0, 0, 0); return f;
+}
+template <> __device__ __forceinline__ Frag<float> frag_zero<float>() {
+  Frag<float> f; f.lo = make_float4(0, 0, 0, 0); f.hi = f.lo; return f;
+}
+
+template <typename T> __device__ __forceinline__ Frag<T> frag_load(const T* p);
+template <> __device__ __forceinline__ Frag<bf16_t> frag_load<bf16_t>(const bf16_t* p) {
+  Frag<bf16_t> f; f.v = *reinterpret_cast<const uint4*>(p); return f;
+}
+template <> __device__ __forceinline__ Frag<float> frag_load<float>(const float* p) {
+  Frag<float> f;
+  f.lo = reinterpret_cast<const float4*>(p)[0];
+  f.hi = reinterpret_cast<const float4*>(p)[1];
+  return f;
+}
+// Streaming load (weights are read once per step): non-temporal hint.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4v_t __attribute__((ext_vector_type(4)));
+template <typename T> __device__ __forceinline__ Frag<T> frag_load_nt(const T* p);
+template <> __device__ __forceinline__ Frag<bf16_t> frag_load_nt<bf16_t>(const bf16_t* p) {
+  u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  Frag<bf16_t> f; f.v = make_uint4(v.x, v.y, v.z, v.w); return f;
+}
+template <> __device__ __forceinline__ Frag<float> frag_load_nt<float>(const float* p) {
+  f32x4v_t a = __builtin_nontemporal_load(reinterpret_cast<const f32x4v_t*>(p));
+  f32x4v_t b = __builtin_nontemporal_load(reinterpret_cast<const f32x4v_t*>(p) + 1);
+  Frag<float> f;
+  f.lo = make_float4(a.x, a.y, a.z, a.w);
+  f.hi = make_float4(b.x, b.y, b.z, b.w);
+  return f;
+}
+
+// acc += A * B for one 16x16 output tile over 32 K-elements (bf16: one
+// v_mfma_f32_16x16x32_bf16) or over 32 K-elements in 8 steps of 4 (f32:
+// v_mfma_f32_16x16x4_f32, element e of every lane in step e).
+__device__ __forceinline__ void mfma(f32x4_t& acc, const Frag<bf16_t>& a, const Frag<bf16_t>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.v),
+                                                __builtin_bit_cast(bf16x8_t, b.v), acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mfma(f32x4_t& acc, const Frag<float>& a, const Frag<float>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.x, b.lo.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.y, b.lo.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.z, b.lo.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.w, b.lo.w, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.x, b.hi.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.y, b.hi.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.z, b.hi.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.w, b.hi.w, acc, 0, 0, 0);
+}
+
+// ---- packed weight layout --------------------------------------------------------
+// W [N][K] (row-major, out x in) is stored as blocks of 16 rows x 128 columns.
+// Block (nt, kc) = rows 16nt.., columns 128kc.., at element offset
+// (nt * KC + kc) * 2048, KC = K / 128.  Inside a block, element
+// [j][lane][e] (j < 4, lane < 64, e < 8) is W[16nt + lane%16][128kc + 32(lane/16) + 8j + e],
+// so load j of a wave reads 64 lanes x 8 elements contiguously and yields the
+// B fragment of one 32-wide MFMA step whose K indices match the A fragment
+// X[row][128kc + 32(lane/16) + 8j + e].
+constexpr int kBlockElems = 2048;
+
+
+// Ordered 64-bit key for a (value, index) maximum: larger value wins, then
+// the lower index.  Keys compare as unsigned integers.
+__device__ __forceinline__ uint64_t argmax_key(float v, uint32_t idx) {
+  uint32_t u = __float_as_uint(v);
+  uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)o << 32) | (uint64_t)(0xFFFFFFFFu - idx);
+}
+__device__ __forceinline__ uint32_t argmax_key_index(uint64_t k) {
+  return 0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFull);
+}
+
+// splitmix64 (Steele, Lea & Flood 2014): first output of the generator whose
+// state is x.
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+__device__ __forceinline__ int32_t pad_id(uint64_t seed, int64_t pos, int32_t vocab) {
+  return (int32_t)(splitmix64(seed ^ ((uint64_t)pos * 0x9E3779B97F4A7C15ull)) % (uint64_t)vocab);
+}
+
+}  // namespace jf

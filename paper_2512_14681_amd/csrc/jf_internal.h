@@ -1,0 +1,107 @@
+// Host-side interface between the C ABI and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace jf {
+
+constexpr int kPage = 64;  // tokens per KV page
+
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_QKV = 2, EPI_SWIGLU = 3, EPI_ARGMAX = 4 };
+
+// What a GEMM does with its output tile Y[R][N] (fp32 accumulators).
+struct Epi {
+  int kind;
+  int R;
+  // EPI_STORE: f32[row * ldf + col] = y;  EPI_RESID: f32[row * ldf + col] += y
+  float* f32;
+  int ldf;
+  // EPI_SWIGLU: columns come in (gate tile, up tile) pairs of 16; writes
+  // act[row * lda + f] = silu(gate) * up, rounded to the element type.
+  void* act;
+  int lda;
+  // EPI_QKV: packed rows are q heads, k heads, v heads (rope pairs (i, i+hd/2)
+  // interleaved 8 by 8 inside each 16-row tile of q and k heads).
+  void* q;                   // [R][H][hd]
+  void* kv;                  // this layer's pages
+  const int32_t* page_table; // logical page -> physical page
+  const int32_t* pos;        // [R] positions (RoPE)
+  const int32_t* state;      // state[0] = committed length C
+  const float* rope_cos;     // [max_ctx][hd/2]
+  const float* rope_sin;
+  int H, G, hd, max_ctx;
+  int32_t* flags;
+  // EPI_ARGMAX: part[blockIdx * R_stride + row] = packed (value, index) max over
+  // the block's columns; optional logits[row * ldl + col] = y.
+  uint64_t* part;
+  int part_stride;
+  float* logits;
+  int ldl;
+};
+
+struct GemmShape {
+  int R, N, K;   // Y[R][N] = X[R][K] * W[N][K]^T
+  int NT, WK;    // 16-column tiles per block, waves splitting K per block
+};
+
+// Chooses NT / WK for a shape (NT fixed by the epilogue where it matters).
+void gemm_plan(GemmShape& s, int epi_kind);
+hipError_t launch_gemm(int dtype, const void* X, int ldx, const void* Wp, const GemmShape& s,
+                       const Epi& ep, hipStream_t stream);
+size_t gemm_blocks(const GemmShape& s);
+
+// Packs W[rows][cols] (row-major) into the kernels' block layout, reading
+// source row rowmap[i] (or i if rowmap is null) from one of up to 4 source
+// matrices: rowmap entries are (src << 24) | row.
+hipError_t launch_pack(int dtype, int rows, int cols, const void* const* srcs, int n_srcs,
+                       const int32_t* d_rowmap, void* dst, hipStream_t stream);
+
+// Tree of one step: parent/pos/vis from segments (row 0 is a root).
+struct SegArgs {
+  int32_t n;
+  int32_t first[16], nrows[16], attach[16], role[16], verify_from[16];
+};
+hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t* flags,
+                       int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t stream);
+
+hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int R, const void* embed,
+                             const float* gamma, int d, int V, float eps, float* h, void* xn,
+                             int32_t* flags, hipStream_t stream);
+hipError_t launch_rmsnorm(int dtype, const float* h, int ldh, int R, const float* gamma, int d,
+                          float eps, void* xn, int ldx, hipStream_t stream);
+
+struct AttnArgs {
+  int H, G, hd, R, max_ctx;
+  int splits;
+  const void* q;             // [R][H][hd]
+  const void* kv;            // this layer's pages
+  const int32_t* page_table;
+  const int32_t* state;      // state[0] = C (device), or null: use C_host
+  int C_host;
+  const uint64_t* vis;       // [R][4] or null (causal)
+  float* o_part;             // [splits][R*H][hd]
+  float* ml_part;            // [splits][R*H][2]
+  void* out;                 // [R][H*hd]
+};
+int attn_splits(int max_keys);
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t stream);
+
+hipError_t launch_argmax_reduce(const uint64_t* part, int nblocks, int stride, int R,
+                                int32_t* g, hipStream_t stream);
+hipError_t launch_accept_linear(const int32_t* draft, const int32_t* g, int n, int mode,
+                                uint64_t seed, int V, const int32_t* state, const int32_t* flags,
+                                int32_t* result, int32_t* next_draft, hipStream_t stream);
+hipError_t launch_accept_tree(const SegArgs& segs, const int32_t* tokens, const int32_t* g,
+                              const int32_t* parent, int R, const int32_t* flags,
+                              int32_t* seg_accept, int32_t* result, int32_t* path,
+                              hipStream_t stream);
+hipError_t launch_commit(int dtype, void* kv, int L, int n_pages, int G, int hd,
+                         const int32_t* page_table, int32_t* state, const int32_t* path,
+                         const int32_t* result, int max_commit, int fixed_count, int max_ctx,
+                         hipStream_t stream);
+hipError_t launch_set_int(int32_t* p, int32_t v, hipStream_t stream);
+hipError_t launch_to_f32(int dtype, const void* src, float* dst, int n, hipStream_t stream);
+hipError_t launch_copy_int(int32_t* dst, const int32_t* src, hipStream_t stream);
+
+}  // namespace jf

@@ -1,0 +1,327 @@
+// The non-GEMM kernels of one Jacobi iteration: the row forest of the step,
+// embedding + RMSNorm, RMSNorm, the vocabulary argmax reduction, greedy
+// acceptance and the KV commit.
+#include "jf_device.h"
+#include "jf_internal.h"
+
+namespace jf {
+
+// ---- a1: rows of the step as a forest (Sec. 3.2, App. A Alg. 1 "Assemble") ----
+// parent[r]: row whose argmax r is checked against (-1: a root, predicted by
+// the last committed row); pos[r] = C + depth(r); vis[r]: bit j set iff row j
+// is r or an ancestor of r.  One thread per row walks its own ancestor chain.
+__global__ void k_tree(SegArgs sg, int R, const int32_t* state, int32_t* flags, int32_t* parent,
+                       int32_t* pos, uint64_t* vis) {
+  __shared__ int32_t par[256];
+  const int r = threadIdx.x;
+  if (r == 0 && flags) *flags = 0;  // flags are per step
+  if (r < R) {
+    int p = -1;
+    for (int s = 0; s < sg.n; ++s) {
+      if (r >= sg.first[s] && r < sg.first[s] + sg.nrows[s]) {
+        p = (r == sg.first[s]) ? sg.attach[s] : r - 1;
+        break;
+      }
+    }
+    par[r] = p;
+  }
+  __syncthreads();
+  if (r < R) {
+    uint64_t w[4] = {0, 0, 0, 0};
+    int depth = 0;
+    int x = r;
+    w[x >> 6] |= 1ull << (x & 63);
+    while (par[x] >= 0) {
+      x = par[x];
+      w[x >> 6] |= 1ull << (x & 63);
+      ++depth;
+    }
+    parent[r] = par[r];
+    pos[r] = state[0] + depth;
+    for (int i = 0; i < 4; ++i) vis[r * 4 + i] = w[i];
+  }
+}
+
+hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t* flags,
+                       int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t st) {
+  if (R < 1 || R > 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_tree, dim3(1), dim3(256), 0, st, segs, R, state, flags, parent, pos, vis);
+  return hipGetLastError();
+}
+
+// ---- block reduction helper --------------------------------------------------
+__device__ __forceinline__ float block_sum(float v, float* sh) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (l == 0) sh[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += sh[i];  // fixed order: deterministic
+  return t;
+}
+
+// ---- a2 + first RMSNorm: h = E[token] (fp32), xn = round(h * rstd * gain) -------
+template <typename T>
+__global__ void k_embed_norm(const int32_t* tokens, const T* E, const float* gamma, int d, int V,
+                             float eps, float* h, T* xn, int32_t* flags) {
+  __shared__ float sh[16];
+  const int r = blockIdx.x;
+  int tok = tokens[r];
+  if (tok < 0 || tok >= V) {
+    if (threadIdx.x == 0 && flags) atomicOr(flags, 1);
+    tok = 0;
+  }
+  const T* e = E + (size_t)tok * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    float v = to_f32<T>(e[i]);
+    h[(size_t)r * d + i] = v;
+    ss += v * v;
+  }
+  ss = block_sum(ss, sh);
+  const float rs = rsqrtf(ss / d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x)
+    xn[(size_t)r * d + i] = from_f32<T>(to_f32<T>(e[i]) * rs * gamma[i]);
+}
+
+hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int R, const void* embed,
+                             const float* gamma, int d, int V, float eps, float* h, void* xn,
+                             int32_t* flags, hipStream_t st) {
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_embed_norm<bf16_t>, dim3(R), dim3(256), 0, st, tokens,
+                       (const bf16_t*)embed, gamma, d, V, eps, h, (bf16_t*)xn, flags);
+  else
+    hipLaunchKernelGGL(k_embed_norm<float>, dim3(R), dim3(256), 0, st, tokens, (const float*)embed,
+                       gamma, d, V, eps, h, (float*)xn, flags);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void k_rmsnorm(const float* h, int ldh, const float* gamma, int d, float eps, T* xn,
+                          int ldx) {
+  __shared__ float sh[16];
+  const int r = blockIdx.x;
+  const float* hr = h + (size_t)r * ldh;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) ss += hr[i] * hr[i];
+  ss = block_sum(ss, sh);
+  const float rs = rsqrtf(ss / d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x)
+    xn[(size_t)r * ldx + i] = from_f32<T>(hr[i] * rs * gamma[i]);
+}
+
+hipError_t launch_rmsnorm(int dtype, const float* h, int ldh, int R, const float* gamma, int d,
+                          float eps, void* xn, int ldx, hipStream_t st) {
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_rmsnorm<bf16_t>, dim3(R), dim3(256), 0, st, h, ldh, gamma, d, eps,
+                       (bf16_t*)xn, ldx);
+  else
+    hipLaunchKernelGGL(k_rmsnorm<float>, dim3(R), dim3(256), 0, st, h, ldh, gamma, d, eps,
+                       (float*)xn, ldx);
+  return hipGetLastError();
+}
+
+// ---- a7 tail: per-row maximum of the LM-head blocks' (value, index) keys ------
+__global__ void k_argmax_reduce(const uint64_t* part, int nblocks, int stride, int32_t* g) {
+  __shared__ uint64_t sh[16];
+  const int r = blockIdx.x;
+  uint64_t best = 0;
+  for (int b = threadIdx.x; b < nblocks; b += blockDim.x) {
+    uint64_t k = part[(size_t)b * stride + r];
+    best = k > best ? k : best;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t other = __shfl_xor(best, o);
+    best = other > best ? other : best;
+  }
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  if (l == 0) sh[w] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) best = sh[i] > best ? sh[i] : best;
+    g[r] = (int32_t)argmax_key_index(best);
+  }
+}
+
+hipError_t launch_argmax_reduce(const uint64_t* part, int nblocks, int stride, int R, int32_t* g,
+                                hipStream_t st) {
+  hipLaunchKernelGGL(k_argmax_reduce, dim3(R), dim3(1024), 0, st, part, nblocks, stride, g);
+  return hipGetLastError();
+}
+
+// ---- a8: greedy acceptance of a linear draft + next draft --------------------------
+// a = 1 + longest run of draft[k] == g[k-1]; pending = g[a-1]; next draft is
+// the Jacobi update g[a-1], g[a], ... padded (mode 1) with pad ids at C+a+i.
+__global__ void k_accept_linear(const int32_t* draft, const int32_t* g, int n, int mode,
+                                uint64_t seed, int V, const int32_t* state, const int32_t* flags,
+                                int32_t* result, int32_t* next_draft) {
+  __shared__ int32_t s_a;
+  __shared__ int32_t gs[256];
+  const int t = threadIdx.x;
+  if (t < n) gs[t] = g[t];
+  if (t == 0) s_a = n;
+  __syncthreads();
+  if (t >= 1 && t < n && draft[t] != gs[t - 1]) atomicMin(&s_a, t);
+  __syncthreads();
+  const int a = s_a;
+  if (t == 0) {
+    result[0] = a;
+    result[1] = 0;
+    result[2] = gs[a - 1];
+    result[3] = flags ? flags[0] : 0;
+  }
+  if (next_draft && t < n) {
+    int src = a - 1 + t;
+    int v;
+    if (src < n) v = gs[src];
+    else v = mode == 1 ? pad_id(seed, (int64_t)state[0] + a + t, V) : 0;
+    next_draft[t] = v;
+  }
+}
+
+hipError_t launch_accept_linear(const int32_t* draft, const int32_t* g, int n, int mode,
+                                uint64_t seed, int V, const int32_t* state, const int32_t* flags,
+                                int32_t* result, int32_t* next_draft, hipStream_t st) {
+  hipLaunchKernelGGL(k_accept_linear, dim3(1), dim3(256), 0, st, draft, g, n, mode, seed, V, state,
+                     flags, result, next_draft);
+  return hipGetLastError();
+}
+
+// ---- a8 (tree): per-segment verification, winner and committed path ------------
+__global__ void k_accept_tree(SegArgs sg, const int32_t* tokens, const int32_t* g,
+                              const int32_t* parent, int R, const int32_t* flags,
+                              int32_t* seg_accept, int32_t* result, int32_t* path) {
+  __shared__ int32_t m[16];
+  const int s = threadIdx.x;
+  if (s < sg.n) {
+    int cnt = 0;
+    for (int i = sg.verify_from[s]; i < sg.nrows[s]; ++i) {
+      int r = sg.first[s] + i;
+      int p = parent[r];
+      if (p >= 0 && tokens[r] == g[p]) ++cnt;
+      else break;
+    }
+    m[s] = cnt;
+    seg_accept[s] = cnt;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int best = 0, bm = m[0];
+    for (int i = 1; i < sg.n; ++i)
+      if (sg.role[i] == 1 && m[i] > bm) { best = i; bm = m[i]; }
+    int k = sg.verify_from[best] + bm;
+    int last = k > 0 ? sg.first[best] + k - 1 : sg.attach[best];
+    if (last < 0) last = 0;  // unreachable for validated segments (row 0 is a root)
+    int len = 0;
+    for (int x = last; x >= 0; x = parent[x]) ++len;
+    int i = len - 1;
+    for (int x = last; x >= 0; x = parent[x]) path[i--] = x;
+    result[0] = len;
+    result[1] = best;
+    result[2] = g[last];
+    result[3] = flags ? flags[0] : 0;
+  }
+}
+
+hipError_t launch_accept_tree(const SegArgs& segs, const int32_t* tokens, const int32_t* g,
+                              const int32_t* parent, int R, const int32_t* flags,
+                              int32_t* seg_accept, int32_t* result, int32_t* path,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(k_accept_tree, dim3(1), dim3(64), 0, st, segs, tokens, g, parent, R, flags,
+                     seg_accept, result, path);
+  return hipGetLastError();
+}
+
+// ---- a9: KV commit ----------------------------------------------------------------
+// The K/V of path row i moves from slot C + path[i] to slot C + i.  path is
+// strictly increasing with path[i] >= i, so walking i upwards never
+// overwrites a source that is still to be read; every (layer, kv head, K|V,
+// dim) column is handled by one thread.
+template <typename T>
+__global__ void k_commit_move(T* kv, int n_pages, int G, int hd, const int32_t* page_table,
+                              const int32_t* state, const int32_t* path, const int32_t* result,
+                              int max_commit) {
+  const int L_idx = blockIdx.y;
+  const int col = blockIdx.x * blockDim.x + threadIdx.x;  // over G * 2 * hd
+  if (col >= G * 2 * hd) return;
+  const int kh = col / (2 * hd), rem = col - kh * 2 * hd, isv = rem / hd, dim = rem - isv * hd;
+  int a = result[0];
+  if (max_commit > 0 && a > max_commit) a = max_commit;
+  const int C = state[0];
+  const size_t page_elems = (size_t)2 * G * kPage * hd;
+  T* base = kv + (size_t)L_idx * n_pages * page_elems;
+  for (int i = 0; i < a; ++i) {
+    int src = C + path[i], dst = C + i;
+    if (src == dst) continue;
+    T* ps = base + (size_t)page_table[src / kPage] * page_elems;
+    T* pd = base + (size_t)page_table[dst / kPage] * page_elems;
+    size_t os, od;
+    if (!isv) {
+      os = ((size_t)kh * kPage + src % kPage) * hd + dim;
+      od = ((size_t)kh * kPage + dst % kPage) * hd + dim;
+    } else {
+      os = (size_t)G * kPage * hd + ((size_t)kh * hd + dim) * kPage + src % kPage;
+      od = (size_t)G * kPage * hd + ((size_t)kh * hd + dim) * kPage + dst % kPage;
+    }
+    pd[od] = ps[os];
+  }
+}
+
+// C += accepted count (capped), or += fixed_count when fixed_count > 0.
+__global__ void k_commit_len(int32_t* state, const int32_t* result, int max_commit,
+                             int fixed_count, int max_ctx) {
+  int a = fixed_count > 0 ? fixed_count : result[0];
+  if (max_commit > 0 && a > max_commit) a = max_commit;
+  int c = state[0] + a;
+  state[0] = c > max_ctx ? max_ctx : c;
+}
+
+hipError_t launch_commit(int dtype, void* kv, int L, int n_pages, int G, int hd,
+                         const int32_t* page_table, int32_t* state, const int32_t* path,
+                         const int32_t* result, int max_commit, int fixed_count, int max_ctx,
+                         hipStream_t st) {
+  if (path) {
+    dim3 grid((G * 2 * hd + 255) / 256, L), block(256);
+    if (dtype == 1)
+      hipLaunchKernelGGL(k_commit_move<bf16_t>, grid, block, 0, st, (bf16_t*)kv, n_pages, G, hd,
+                         page_table, state, path, result, max_commit);
+    else
+      hipLaunchKernelGGL(k_commit_move<float>, grid, block, 0, st, (float*)kv, n_pages, G, hd,
+                         page_table, state, path, result, max_commit);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_commit_len, dim3(1), dim3(1), 0, st, state, result, max_commit, fixed_count,
+                     max_ctx);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void k_to_f32(const T* src, float* dst, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    dst[i] = to_f32<T>(src[i]);
+}
+
+hipError_t launch_to_f32(int dtype, const void* src, float* dst, int n, hipStream_t st) {
+  dim3 grid((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024), block(256);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_to_f32<bf16_t>, grid, block, 0, st, (const bf16_t*)src, dst, n);
+  else
+    hipLaunchKernelGGL(k_to_f32<float>, grid, block, 0, st, (const float*)src, dst, n);
+  return hipGetLastError();
+}
+
+__global__ void k_set_int(int32_t* p, int32_t v) { *p = v; }
+__global__ void k_copy_int(int32_t* d, const int32_t* s) { *d = *s; }
+
+hipError_t launch_set_int(int32_t* p, int32_t v, hipStream_t st) {
+  hipLaunchKernelGGL(k_set_int, dim3(1), dim3(1), 0, st, p, v);
+  return hipGetLastError();
+}
+hipError_t launch_copy_int(int32_t* d, const int32_t* s, hipStream_t st) {
+  hipLaunchKernelGGL(k_copy_int, dim3(1), dim3(1), 0, st, d, s);
+  return hipGetLastError();
+}
+
+}  // namespace jf

@@ -1,0 +1,196 @@
+"""GPU parity on the tiny fp32 decoder (2 layers, d 128, 4 heads of 32,
+FFN 512, V 1024): every call goes through the C ABI of libjf and is checked
+against the CPU oracle on the same seeded inputs.
+
+Tolerances: the model is fp32 end to end, so logits must agree with the
+oracle's fp64 values within 1e-4 absolute; tokens must be identical except
+where the oracle's top-2 logit gap is below 1e-3.
+"""
+import numpy as np
+import pytest
+
+import jf_inputs
+from oracle import jacobi as ojac
+from oracle import multiblock as omb
+from oracle.model import DecoderOracle
+
+pytestmark = pytest.mark.gpu
+
+SHAPE = jf_inputs.MODEL_SHAPES["tiny"]
+LOGIT_TOL = 1e-4
+GAP_EXEMPT = 1e-3
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    from paper_2512_14681_amd import decode, jf
+    assert torch.cuda.is_available()
+    w = jf_inputs.model_weights(SHAPE, seed=0)
+    prompt = jf_inputs.prompt(1, 32, SHAPE["vocab"])
+    model = jf.Model(SHAPE, w, max_rows=64, max_ctx=512)
+    return dict(w=w, prompt=prompt, model=model, dec=decode.Decoder(model), jf=jf, torch=torch)
+
+
+def oracle(env):
+    return ojac.TransformerBackend(DecoderOracle(SHAPE, env["w"]))
+
+
+def test_prefill_pending_matches(env):
+    env["dec"].reset()
+    p = env["dec"].prefill(env["prompt"])
+    be = oracle(env)
+    assert p == be.prefill(env["prompt"])
+
+
+@pytest.mark.parametrize("n", [1, 5, 16, 17, 33, 64])
+def test_step_logits_and_argmax(env, n):
+    """One linear step of n rows (several 16-row tiles and a ragged tail)."""
+    import torch
+    dec, jf_ = env["dec"], env["jf"]
+    dec.reset()
+    p = dec.prefill(env["prompt"])
+    draft = [p] + [ojac.pad_id(7, 32 + i, SHAPE["vocab"]) for i in range(1, n)]
+    d_draft = torch.tensor(draft, dtype=torch.int32, device="cuda")
+    d_next = torch.zeros(n, dtype=torch.int32, device="cuda")
+    d_logits = torch.empty((n, SHAPE["vocab"]), dtype=torch.float32, device="cuda")
+    env["model"].jf_jacobi_step(d_draft, n, 1, 7, dec.d_argmax, dec.d_result, d_next, d_logits)
+    torch.cuda.synchronize()
+    z = d_logits.cpu().numpy()
+    g = dec.d_argmax[:n].cpu().numpy()
+    res = dec.d_result.cpu().numpy()
+    be = oracle(env)
+    be.prefill(env["prompt"])
+    gz, _ = be.step(draft, ojac.linear_segments(n))
+    zo = be.last[1]
+    assert np.abs(z - zo).max() < LOGIT_TOL
+    gap = be.log[-1]["gap"]
+    ok = (g == gz) | (gap < GAP_EXEMPT)
+    assert ok.all()
+    a = ojac.accept_linear(draft, gz)
+    assert res[0] == a and res[2] == gz[a - 1] and res[3] == 0
+    # window-mode next draft: Jacobi update then pad ids after the new length
+    nxt = list(gz[a - 1:]) + [ojac.pad_id(7, 32 + a + i, SHAPE["vocab"]) for i in range(n - a + 1, n)]
+    assert list(d_next.cpu().numpy()) == nxt
+
+
+def test_block_mode_64_tokens_equals_ar(env):
+    """Configuration 1: block n = 8, random draft init, 64 new tokens."""
+    dec = env["dec"]
+    dec.reset()
+    got, acc = dec.generate_jacobi(env["prompt"], 8, 64, mode="block", pad_seed=2)
+    want = ojac.generate_ar(oracle(env), env["prompt"], 64)
+    assert got == want
+    _, acc_o = ojac.generate_jacobi(oracle(env), env["prompt"], 8, 64, "block", pad_seed=2)
+    assert acc == acc_o
+    assert all(a >= 1 for a in acc)
+
+
+@pytest.mark.parametrize("n,mode", [(1, "window"), (8, "window"), (16, "window"), (3, "block")])
+def test_other_modes_equal_ar(env, n, mode):
+    dec = env["dec"]
+    dec.reset()
+    got, acc = dec.generate_jacobi(env["prompt"], n, 40, mode=mode, pad_seed=5)
+    want = ojac.generate_ar(oracle(env), env["prompt"], 40)
+    assert got == want
+    _, acc_o = ojac.generate_jacobi(oracle(env), env["prompt"], n, 40, mode, pad_seed=5)
+    assert acc == acc_o
+
+
+def test_gpu_ar_driver(env):
+    dec = env["dec"]
+    dec.reset()
+    assert dec.generate_ar(env["prompt"], 20) == ojac.generate_ar(oracle(env), env["prompt"], 20)
+
+
+def test_multiblock_lockstep(env):
+    """Same policy, same model: the GPU and oracle multi-block runs take the
+    same steps (rows, per-segment accepts, winner, committed tokens)."""
+    dec = env["dec"]
+    dec.reset()
+    got, tr = dec.generate_multiblock(env["prompt"], 8, 3, 0.5, 48, pad_seed=3)
+    want, tro = omb.generate_multiblock(oracle(env), env["prompt"], 8, 3, 0.5, 48, pad_seed=3)
+    assert got == want == ojac.generate_ar(oracle(env), env["prompt"], 48)
+    assert len(tr) == len(tro)
+    for a, b in zip(tr, tro):
+        assert (a["R"], a["m"], a["winner"], a["a"], a["committed"]) == \
+               (b["R"], b["m"], b["winner"], b["a"], b["committed"])
+    assert max(t["R"] for t in tr) > 8  # pseudo blocks were in play
+
+
+def test_prefill_chunks_longer_than_max_rows(env):
+    import torch
+    from paper_2512_14681_amd import decode, jf
+    prompt = jf_inputs.prompt(11, 100, SHAPE["vocab"])
+    m = jf.Model(SHAPE, env["w"], max_rows=16, max_ctx=256)
+    dec = decode.Decoder(m)
+    got = dec.generate_jacobi(prompt, 16, 24, mode="window")[0]
+    assert got == ojac.generate_ar(oracle(env), prompt, 24)
+    assert dec.length() == 100 + 24
+
+
+def test_permuted_page_table_same_tokens(env):
+    from paper_2512_14681_amd import decode, jf
+    m = jf.Model(SHAPE, env["w"], max_rows=16, max_ctx=256)
+    m.jf_kv_set_page_table(np.array([3, 1, 0, 2], dtype=np.int32))
+    dec = decode.Decoder(m)
+    got = dec.generate_jacobi(env["prompt"], 8, 64, mode="window")[0]
+    assert got == ojac.generate_ar(oracle(env), env["prompt"], 64)
+
+
+def test_error_paths(env):
+    import torch
+    jf_ = env["jf"]
+    from paper_2512_14681_amd import decode, jf
+    m = jf.Model(SHAPE, env["w"], max_rows=16, max_ctx=128)
+    dec = decode.Decoder(m)
+    d = torch.zeros(32, dtype=torch.int32, device="cuda")
+    with pytest.raises(jf.JfError) as e:
+        m.jf_jacobi_step(d, 4, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
+    assert e.value.status == jf.JF_E_STATE          # no prefill yet
+    with pytest.raises(jf.JfError) as e:
+        m.jf_commit_kv(None, dec.d_result)
+    assert e.value.status == jf.JF_E_STATE          # nothing to commit
+    dec.prefill(env["prompt"])
+    with pytest.raises(jf.JfError) as e:
+        m.jf_jacobi_step(d, 17, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
+    assert e.value.status == jf.JF_E_CAPACITY       # n > max_rows
+    with pytest.raises(jf.JfError) as e:
+        m.jf_jacobi_step(d, 4, 2, 0, dec.d_argmax, dec.d_result, dec.d_next)
+    assert e.value.status == jf.JF_E_INVAL          # bad mode
+    bad = [[(0, 3, -1, 0, 1), (4, 1, 0, 1, 0)],     # gap in rows
+           [(0, 3, 0, 0, 1)],                       # first not a root
+           [(0, 2, -1, 1, 1)],                      # first not real-active
+           [(0, 2, -1, 0, 1), (2, 2, 2, 1, 0)]]     # attaches forward
+    for segs in bad:
+        R = sum(s[1] for s in segs)
+        with pytest.raises(jf.JfError) as e:
+            m.jf_multiblock_step(d, R, segs, dec.d_argmax, dec.d_seg, dec.d_result, dec.d_path)
+        assert e.value.status == jf.JF_E_INVAL
+    with pytest.raises(jf.JfError) as e:
+        m.jf_kv_truncate(1000)
+    assert e.value.status == jf.JF_E_STATE
+    # capacity: perfect drafts (the AR tokens) commit all 16 rows per step;
+    # 32 + 6 * 16 = 128 = max_ctx, so a seventh step has no room
+    ar = ojac.generate_ar(oracle(env), env["prompt"], 112)
+    for i in range(6):
+        d[:16] = torch.tensor(ar[16 * i:16 * i + 16], dtype=torch.int32)
+        m.jf_jacobi_step(d, 16, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
+        m.jf_commit_kv(None, dec.d_result)
+        assert dec.d_result.cpu()[0] == 16
+    assert m.jf_kv_length() == 128
+    with pytest.raises(jf.JfError) as e:
+        m.jf_jacobi_step(d, 16, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
+    assert e.value.status == jf.JF_E_CAPACITY
+    # max_commit caps what a commit keeps
+    m.jf_kv_truncate(32)
+    d[:16] = torch.tensor(ar[:16], dtype=torch.int32)
+    m.jf_jacobi_step(d, 16, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
+    m.jf_commit_kv(None, dec.d_result, 5)
+    assert m.jf_kv_length() == 37
+    # out-of-range token ids are flagged by the device, never read out of bounds
+    m.jf_kv_truncate(32)
+    d[:4] = torch.tensor([5, 2000, -3, 7], dtype=torch.int32)
+    m.jf_jacobi_step(d, 4, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
+    res = dec.d_result.cpu().numpy()
+    assert res[3] & jf.JF_FLAG_BAD_TOKEN
