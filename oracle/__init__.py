@@ -18,7 +18,7 @@ Contents, each citing the passage it follows:
                     blocks concatenated; App. A, Alg. 1 "Assemble").
 * ``jacobi``     -- greedy AR decoding (Eq. 1), the Jacobi update (Eq. 3),
                     longest-prefix acceptance, block mode (Eq. 4), running
-                    window (Sec. 4 "multi-block ... running window") and the
+                    window (Sec. 4.2, running-window variant) and the
                     pure fixed-point iteration of Eq. 3 without commits.
 * ``multiblock`` -- multi-block decoding with rejection recycling (Sec. 3.2,
                     App. A Alg. 1).

@@ -20,7 +20,7 @@ a draft d[0..n-1] with d[0] = p at positions C..C+n-1:
 which is the greedy acceptance of Sec. 3.2 / App. A Alg. 1 ("accept longest
 matching prefix").  The next draft is the Jacobi update of the rest,
 [g[a-1], g[a], ...]: truncated to what is left of the block (block mode,
-Eq. 4) or padded back to n (running window, Sec. 4 "running window").
+Eq. 4) or padded back to n (running window, Sec. 4.2).
 
 Draft initialisation ("randomly initialise", Sec. 1 and Eq. 3) draws
 pad_id(seed, pos) = splitmix64(seed XOR pos * 0x9E3779B97F4A7C15) mod V, the
