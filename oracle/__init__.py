@@ -8,8 +8,8 @@ import it; the product path never does and shares no code with it.
 
 Contents, each citing the passage it follows:
 
-* ``numerics``   -- bf16 round-to-nearest-even emulation (rounding points of
-                    the bf16 model variant; not a paper passage).
+* ``numerics``   -- bf16 round-to-nearest-even emulation (the bf16 KV cache
+                    of the bf16 model variant; not a paper passage).
 * ``model``      -- the decoder forward pass over draft rows against an exact
                     prefix KV cache (Sec. 2.1 "Jacobi Decoding": one forward
                     pass under a causal mask yields every row's prediction).

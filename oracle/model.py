@@ -8,17 +8,24 @@ committed prefix (Sec. 1).  This module is that decoder written out plainly:
 
     h     = E[token]
     per layer:
-      xn  = RMSNorm(h) * g_attn                    (bf16-rounded in bf16 mode)
+      xn  = RMSNorm(h) * g_attn
       q,k,v = xn Wq^T, xn Wk^T, xn Wv^T
       q,k = RoPE(q, pos), RoPE(k, pos)             (rotate-half pairing i, i+hd/2)
-      q,k,v rounded (bf16 mode); k,v are what the cache stores
+      k,v are what the cache stores (rounded to bf16 in bf16 mode)
       o   = softmax(q k^T / sqrt(hd)) v over the visible keys, GQA with query
-            head j reading KV head floor(j / (H/G))  (o rounded in bf16 mode)
+            head j reading KV head floor(j / (H/G))
       h   = h + o Wo^T
-      u   = RMSNorm(h) * g_ffn                     (rounded in bf16 mode)
-      m   = silu(u Wg^T) * (u Wu^T)                (rounded in bf16 mode)
+      u   = RMSNorm(h) * g_ffn
+      m   = silu(u Wg^T) * (u Wu^T)
       h   = h + m Wd^T
-    logits = (RMSNorm(h) * g_final, rounded) W_lm^T
+    logits = (RMSNorm(h) * g_final) W_lm^T
+
+bf16 mode means bf16 weights and a bf16 KV cache; every other value is
+computed in the oracle's precision (fp64 by default).  Rounding activations
+to bf16 as well would make any two correct implementations disagree by
+random 1-ulp flips that compound layer after layer (the logits of a
+2-layer d=2048 model then differ by up to 2e-2 between fp32 and fp64
+arithmetic), so the engine carries activations in fp32.
 
 Visible keys of a row: the whole committed prefix [0, C) plus the in-step
 rows marked in its visibility row (its ancestors and itself).
@@ -163,22 +170,22 @@ class DecoderOracle:
         kv_rows = []
         for l in range(self.L):
             p = f"layers.{l}."
-            xn = self.rnd(self.rmsnorm(h, self.w(p + "attn_norm")))
+            xn = self.rmsnorm(h, self.w(p + "attn_norm"))
             q = self.mm(xn, self.w(p + "wq")).reshape(R, H, hd)
             k = self.mm(xn, self.w(p + "wk")).reshape(R, G, hd)
             v = self.mm(xn, self.w(p + "wv")).reshape(R, G, hd)
-            q = self.rnd(self.rope(q, pos))
-            k = self.rnd(self.rope(k, pos))
+            q = self.rope(q, pos)
+            k = self.rnd(self.rope(k, pos))     # the cache holds bf16 K/V
             v = self.rnd(v)
             kv_rows.append((k, v))
-            o = self.rnd(self.attention(l, q, k, v, vis)).reshape(R, H * hd)
+            o = self.attention(l, q, k, v, vis).reshape(R, H * hd)
             h = h + self.mm(o, self.w(p + "wo"))
-            u = self.rnd(self.rmsnorm(h, self.w(p + "ffn_norm")))
+            u = self.rmsnorm(h, self.w(p + "ffn_norm"))
             gt = self.mm(u, self.w(p + "w_gate"))
             up = self.mm(u, self.w(p + "w_up"))
-            m = self.rnd(gt / (1.0 + np.exp(-gt)) * up)
+            m = gt / (1.0 + np.exp(-gt)) * up
             h = h + self.mm(m, self.w(p + "w_down"))
-        xf = self.rnd(self.rmsnorm(h, self.w("final_norm")))
+        xf = self.rmsnorm(h, self.w("final_norm"))
         logits = self.mm(xf, self.w("lm_head"))
         return logits, kv_rows
 

@@ -1,9 +1,9 @@
 """bf16 emulation for the oracle (rounding points of the bf16 model variant).
 
-The paper fixes no precision.  The bf16 variant rounds the inputs of every
-weight contraction and the cached K/V to bf16; this module rounds float64 or
-float32 values to the nearest bf16 value (ties to even), returned in the input
-dtype, using integer operations on the IEEE bit patterns.
+The paper fixes no precision.  The bf16 variant stores weights and the
+cached K/V in bf16; this module rounds float64 or float32 values to the
+nearest bf16 value (ties to even), returned in the input dtype, using integer
+operations on the IEEE bit patterns.
 """
 import numpy as np
 

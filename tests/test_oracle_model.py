@@ -127,8 +127,8 @@ def test_rmsnorm_closed_form():
 
 
 def test_bf16_mode_rounding_points():
-    """bf16 model: cached K/V are bf16 values and logits stay close to the
-    unrounded computation on the same bf16 weights."""
+    """bf16 model: cached K/V are bf16 values, the rest is unrounded, so the
+    logits stay close to a run without the cache rounding."""
     shape = dict(SMALL, dtype="bf16")
     w = jf_inputs.model_weights(shape, seed=8)
     toks = jf_inputs.prompt(9, 12, shape["vocab"])
