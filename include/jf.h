@@ -58,17 +58,33 @@ typedef enum { JF_F32 = 0, JF_BF16 = 1 } jf_dtype;
  * inverse frequency rope_base^(-2i/head_dim)), grouped-query attention with
  * query head j reading KV head j / (n_heads / n_kv_heads), SwiGLU FFN,
  * untied LM head, no biases.
- * Limits: d_model, d_ffn multiples of 128; head_dim in {32, 64, 128};
+ * Limits: d_model, d_ffn multiples of 128, d_model <= 4096; head_dim in
+ * {32, 64, 128};
  * n_heads * head_dim a multiple of 128; n_heads a multiple of n_kv_heads;
  * vocab a multiple of 16; 1 <= max_rows <= 256; max_ctx a multiple of 64. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
   float rope_base, rms_eps;
-  int32_t dtype;     /* jf_dtype of weights, GEMM inputs and the KV cache;
-                        the residual stream, softmax and logits are fp32   */
+  int32_t dtype;     /* jf_dtype of the weights and the KV cache; all
+                        activations are fp32 (see "activation planes")     */
   int32_t max_rows;  /* largest number of rows of any step / prefill chunk */
   int32_t max_ctx;   /* KV cache capacity in tokens                         */
 } jf_config;
+
+/* Activation planes: an activation tensor A[...] of a JF_BF16 model is kept
+ * as two bf16 planes, hi = bf16(A) then lo = bf16(A - hi) (A ~= hi + lo to
+ * about 16 significant bits); a JF_F32 model keeps one fp32 plane.  Either
+ * way 4 bytes per element.  The component calls below take and return
+ * activations in this form.
+ *
+ * GEMM-input layout: an activation matrix that feeds a projection, X[R][K]
+ * (K a multiple of 128), is stored with R padded to Rp = 16 * ceil(R / 16)
+ * rows as 16-row tiles, each a run of 128-column blocks; inside a 16 x 128
+ * block, element (r, c) sits at j * 512 + lane * 8 + e, lane = r + 16 (c/32),
+ * j = (c % 32) / 8, e = c % 8 (the matrix-core operand order, so one
+ * fragment load is one contiguous 1 KB).  Element (row, col) of X is at
+ *   ((row / 16) * (K / 128) + col / 128) * 2048 + that in-block offset,
+ * and the lo plane follows the hi plane Rp * K elements later. */
 
 /* One chain of rows in a multi-block step (App. A Alg. 1 "Assemble").
  * Rows first_row .. first_row+n_rows-1 form a chain; the first hangs under
@@ -189,15 +205,34 @@ jf_status jf_kv_truncate(jf_model *m, int32_t new_len, jf_stream stream);
 jf_status jf_kv_set_page_table(jf_model *m, const int32_t *h_table,
                                int32_t n, jf_stream stream);
 
+/* ---- measurement ---------------------------------------------------------
+ * Kernel classes of one step; jf_profile_begin makes every following launch
+ * of that class on this model bracketed by two HIP events on the launch
+ * stream, jf_profile_end synchronises, returns the summed event time (ms)
+ * and the number of launches, and stops recording. */
+enum {
+  JF_KERNEL_QKV = 1,    /* RMSNorm'd x times W_qkv, RoPE, K/V into the cache */
+  JF_KERNEL_ATTN = 2,   /* attention + split combine                         */
+  JF_KERNEL_O = 3,      /* O projection + residual                           */
+  JF_KERNEL_GATEUP = 4, /* gate/up projection + SwiGLU                       */
+  JF_KERNEL_DOWN = 5,   /* down projection + residual                        */
+  JF_KERNEL_LMHEAD = 6, /* LM head + per-block argmax                        */
+  JF_KERNEL_STEP = 7    /* a whole jf_jacobi_step / jf_multiblock_step       */
+};
+jf_status jf_profile_begin(jf_model *m, int32_t kernel_class);
+jf_status jf_profile_end(jf_model *m, double *total_ms, int32_t *launches);
+
 /* ---- component calls (used by the attention and LM-head workloads) ---- */
 
 /* Attention of one layer (the attention inside Eq. 3's forward pass):
- * q [R][n_heads][head_dim] (dtype), keys/values of positions 0..C+R-1 in one
- * layer's paged cache d_kv_layer (layout as in jf_model_load), with the
- * page table d_page_table.  Row r sees positions [0, C) and in-step position
- * C + j iff bit j of d_vis[r][4] is set (d_vis NULL: j <= r, causal).
- * out [R][n_heads][head_dim] (dtype).  d_ws of at least
- * jf_attention_ws_bytes(...). */
+ * q [R][n_heads][head_dim] activation planes, keys/values of positions
+ * 0..C+R-1 in one layer's paged cache d_kv_layer (layout as in
+ * jf_model_load; slots beyond C+R in a used page must hold finite values),
+ * with the page table d_page_table.  Row r sees positions [0, C) and
+ * in-step position C + j iff bit j of d_vis[r][4] is set (d_vis NULL:
+ * j <= r, causal).  out: activation planes of the [R][n_heads * head_dim]
+ * matrix in the GEMM-input layout (the O projection's input), Rp * n_heads *
+ * head_dim elements per plane.  d_ws of at least jf_attention_ws_bytes(...). */
 size_t jf_attention_ws_bytes(int32_t n_heads, int32_t head_dim, int32_t R);
 jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
                        int32_t dtype, int32_t C, int32_t R, const void *d_q,
@@ -206,10 +241,17 @@ jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
                        jf_stream stream);
 
 /* LM head + greedy argmax + longest-prefix acceptance (Eq. 3, Alg. 1
- * "Verification"): x [R][d] (dtype) times lm_head^T, lm_head packed by
- * jf_pack_matrix; g = argmax per row (lowest id on ties); accept as in
+ * "Verification"): x [R][d] activation planes in the GEMM-input layout
+ * (Rp * d elements per plane) times lm_head^T (dtype), lm_head [V][d]
+ * packed by jf_pack_matrix; g = argmax per row (lowest id on ties); accept as in
  * jf_jacobi_step against d_draft[R] (NULL: no acceptance, d_result unused).
- * d_ws of at least jf_lm_head_ws_bytes(R, V). */
+ * d_ws of at least jf_lm_head_ws_bytes(R, V).
+ * Packed weight layout (jf_pack_matrix): W[rows][cols] (rows % 16 == 0,
+ * cols % 128 == 0) as 16 x 128 blocks in the same in-block order as the
+ * GEMM-input layout (row r of the block = W row, c = W column); 16-row tiles
+ * come in groups of P = 4 (rows % 64 == 0), else 2 (rows % 32 == 0), else 1,
+ * and block (tile t, column block kc) is block number
+ * ((t / P) * (cols / 128) + kc) * P + t % P. */
 size_t jf_packed_matrix_bytes(int32_t rows, int32_t cols, int32_t dtype);
 jf_status jf_pack_matrix(int32_t rows, int32_t cols, int32_t dtype,
                          const void *d_src, void *d_packed, jf_stream stream);

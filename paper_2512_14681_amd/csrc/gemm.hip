@@ -9,15 +9,18 @@
 // 16-row tile of X.  A workgroup owns NT adjacent 16-column tiles and splits
 // K over WK waves; the waves' partial tiles are summed in LDS in a fixed
 // order (deterministic) and the epilogue runs on the reduced tile.
+#include <algorithm>
+
 #include "jf_device.h"
 #include "jf_internal.h"
 
 namespace jf {
 
+// Runs on the reduced output tile of column group ng (NT * 16 columns),
+// tile[row * tld + c], with threads tid = 0..nth-1 sharing the work.
 template <typename T>
-__device__ __forceinline__ void epilogue(const float* tile, int tld, int RT, int NT, const Epi& ep) {
-  const int tid = threadIdx.x, nth = blockDim.x;
-  const int ng = blockIdx.x;
+__device__ __forceinline__ void epilogue(const float* tile, int tld, int NT, const Epi& ep, int ng,
+                                         int tid, int nth) {
   const int cols = NT * 16;
   const int R = ep.R;
   if (ep.kind == EPI_STORE || ep.kind == EPI_RESID) {
@@ -36,7 +39,7 @@ __device__ __forceinline__ void epilogue(const float* tile, int tld, int RT, int
       float gt = tile[row * tld + (2 * p) * 16 + c];
       float up = tile[row * tld + (2 * p + 1) * 16 + c];
       float s = gt / (1.0f + __expf(-gt));
-      act[(size_t)row * ep.lda + (size_t)ng * half_cols + f] = from_f32<T>(s * up);
+      act_store<T>(act + act_offset(row, ng * half_cols + f, ep.act_k), ep.act_plane, s * up);
     }
   } else if (ep.kind == EPI_ARGMAX) {
     for (int row = tid; row < R; row += nth) {
@@ -79,10 +82,10 @@ __device__ __forceinline__ void epilogue(const float* tile, int tld, int RT, int
         dim = w;
         out = x;
       }
-      T v = from_f32<T>(out);
       if (head < H) {
-        q[((size_t)row * H + head) * hd + dim] = v;
+        act_store<T>(q + ((size_t)row * H + head) * hd + dim, ep.q_plane, out);
       } else {
+        const T v = from_f32<T>(out);
         int slot = C + row;
         if (slot >= ep.max_ctx) {
           if (ep.flags) atomicOr(ep.flags, 2);
@@ -103,15 +106,36 @@ __device__ __forceinline__ void epilogue(const float* tile, int tld, int RT, int
   }
 }
 
-template <typename T, int RT, int NT, int WK>
+// Register ring: D K-blocks of weights (and, for <= 32 rows, of
+// activations) are in flight per wave.  The default depth is the largest
+// (<= 4) that fits a register budget leaving room for two waves per SIMD
+// (512 registers per lane per SIMD), or for the whole block when it has more
+// than 8 waves.
+template <typename T, int RT, int NT, int WK> struct Ring {
+  static constexpr bool kPrefetchX = RT <= 2;
+  static constexpr int kBudget = WK <= 8 ? 224 : 112;
+  static constexpr int kFragRegs = sizeof(T) == 2 ? 4 : 8;
+  static constexpr int kFixed = 48 + RT * NT * 4 + (kPrefetchX ? 0 : 4 * 8);
+  static constexpr int kPerSlot = NT * 4 * kFragRegs + (kPrefetchX ? RT * 4 * 8 : 0);
+  static constexpr int kD = (kBudget - kFixed) / kPerSlot;
+  static constexpr int D = kD < 1 ? 1 : (kD > 4 ? 4 : kD);
+};
+
+template <typename T, int RT, int NT, int WK, int D = Ring<T, RT, NT, WK>::D>
 __global__ void __launch_bounds__(64 * WK)
-k_gemm(const T* __restrict__ X, int ldx, const T* __restrict__ Wp, int KC, Epi ep) {
+k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC, int P, Epi ep) {
   extern __shared__ float lds[];
+  constexpr bool PX = Ring<T, RT, NT, WK>::kPrefetchX;
+  constexpr int RX = PX ? RT : 1;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int ng = blockIdx.x;
+  const int ks = blockIdx.y, S = gridDim.y;
   const int R = ep.R;
-  const int kc0 = (KC * wave) / WK, kc1 = (KC * (wave + 1)) / WK;
+  const int kb0 = (KC * ks) / S, kb1 = (KC * (ks + 1)) / S;   // this block's K-blocks
+  const int kc0 = kb0 + ((kb1 - kb0) * wave) / WK;
+  const int kc1 = kb0 + ((kb1 - kb0) * (wave + 1)) / WK;
+  const int nk = kc1 - kc0;
 
   f32x4_t acc[RT][NT];
 #pragma unroll
@@ -121,28 +145,80 @@ k_gemm(const T* __restrict__ X, int ldx, const T* __restrict__ Wp, int KC, Epi e
 
   const int lrow = lane & 15;
   const int koff = (lane >> 4) * 32;
-  const T* wb = Wp + (size_t)(ng * NT) * KC * kBlockElems + lane * 8;
+  // Packed layout: tiles in groups of P, K-block-major inside a group, so a
+  // wave whose NT tiles form (part of) one group streams one contiguous run.
+  const T* wb = Wp + lane * 8;
+  size_t toff[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int t = ng * NT + nt;
+    toff[nt] = ((size_t)(t / P) * KC * P + t % P) * kBlockElems;
+  }
+  const size_t kstride = (size_t)P * kBlockElems;
+  // Rows past R read row R-1 instead (no per-lane branch): MFMA rows are
+  // independent and padding rows are never stored.
+  auto xload = [&](int kc, int mt, ActFrag<T> (&x)[4]) {
+    const int row = min(mt * 16 + lrow, R - 1);
+    const T* xp = X + act_offset(row, kc * 128 + koff, KC * 128);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = act_load<T>(xp + j * 512, xplane);
+  };
 
-
-  for (int kc = kc0; kc < kc1; ++kc) {
-    Frag<T> b[NT][4];
+  // Slot d holds the weights (and activations) of one 128-wide K-block; it
+  // is refilled with the block D ahead as soon as it has been consumed.
+  Frag<T> wr[D][NT][4];
+  ActFrag<T> xr[D][RX][4];
+  auto load = [&](int kc, Frag<T> (&w)[NT][4], ActFrag<T> (&x)[RX][4]) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        b[nt][j] = frag_load_nt<T>(wb + ((size_t)nt * KC + kc) * kBlockElems + j * 512);
+        w[nt][j] = frag_load_nt<T>(wb + toff[nt] + kc * kstride + j * 512);
+    if constexpr (PX) {
+#pragma unroll
+      for (int mt = 0; mt < RT; ++mt) xload(kc, mt, x[mt]);
+    }
+  };
+  auto compute = [&](int kc, const Frag<T> (&w)[NT][4], const ActFrag<T> (&x)[RX][4]) {
 #pragma unroll
     for (int mt = 0; mt < RT; ++mt) {
-      const int row = mt * 16 + lrow;
-      const T* xp = X + (size_t)row * ldx + kc * 128 + koff;
+      ActFrag<T> xt[4];
+      if constexpr (PX) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        Frag<T> a = row < R ? frag_load<T>(xp + j * 8) : frag_zero<T>();
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) mfma(acc[mt][nt], a, b[nt][j]);
+        for (int j = 0; j < 4; ++j) xt[j] = x[mt][j];
+      } else {
+        xload(kc, mt, xt);
       }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) mfma(acc[mt][nt], xt[j], w[nt][j]);
+    }
+  };
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+    if (d < nk) load(kc0 + d, wr[d], xr[d]);
+  int base = 0;
+  // Steady state with no conditions inside, so the compiler keeps the other
+  // D-1 slots' loads in flight while one slot is consumed.
+  for (; base + 2 * D <= nk; base += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      compute(kc0 + base + d, wr[d], xr[d]);
+      load(kc0 + base + D + d, wr[d], xr[d]);
     }
   }
+  // Tail: fewer than 2D blocks left, the first min(D, nk - base) in flight.
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    if (base + d < nk) {
+      compute(kc0 + base + d, wr[d], xr[d]);
+      if (base + D + d < nk) load(kc0 + base + D + d, wr[d], xr[d]);
+    }
+  }
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+    if (base + D + d < nk) compute(kc0 + base + D + d, wr[d], xr[d]);
 
   // Output tile [RT*16][NT*16] in LDS after the partials (if any).
   const int tld = NT * 16 + 1;
@@ -175,7 +251,51 @@ k_gemm(const T* __restrict__ X, int ldx, const T* __restrict__ Wp, int KC, Epi e
     }
   }
   __syncthreads();
-  epilogue<T>(tile, tld, RT, NT, ep);
+  if (S > 1) {
+    // Split-K over blocks: publish this block's partial tile; the block that
+    // arrives last for this column group sums all partials in split order
+    // (deterministic) and runs the epilogue, then re-arms the counter.
+    // Partials travel with device-coherent (agent-scope) stores and loads,
+    // which bypass the per-XCD L2, so no L2 write-back / invalidate fence is
+    // needed: the stores are complete (s_waitcnt) before the counter
+    // increment, and the last block reads them after seeing the count.
+    __shared__ int s_last;
+    const int cols = NT * 16;
+    float* mine = ep.kpart + ((size_t)ng * S + ks) * (size_t)(R * cols);
+    for (int e = threadIdx.x; e < R * cols; e += 64 * WK) {
+      const int row = e / cols, c = e - row * cols;
+      __hip_atomic_store(mine + e, tile[row * tld + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's stores are done
+    __syncthreads();
+    if (threadIdx.x == 0)
+      s_last = __hip_atomic_fetch_add(ep.kcount + ng, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+    __syncthreads();
+    if (!s_last) return;
+    // Loads are issued four splits at a time so that their latencies
+    // overlap; the sum keeps split order.
+    const float* all = ep.kpart + (size_t)ng * S * (size_t)(R * cols);
+    const size_t pstride = (size_t)R * cols;
+    for (int e = threadIdx.x; e < R * cols; e += 64 * WK) {
+      float sum = 0.f;
+      int k = 0;
+      for (; k + 4 <= S; k += 4) {
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          v[i] = __hip_atomic_load(all + (k + i) * pstride + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sum += v[i];
+      }
+      for (; k < S; ++k)
+        sum += __hip_atomic_load(all + k * pstride + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int row = e / cols, c = e - row * cols;
+      tile[row * tld + c] = sum;
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(ep.kcount + ng, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+  }
+  epilogue<T>(tile, tld, NT, ep, ng, threadIdx.x, blockDim.x);
 }
 
 static int round_rt(int R) {
@@ -193,73 +313,130 @@ static size_t lds_bytes(int RT, int NT, int WK) {
   return ((WK > 1 ? WK * part : 0) + tile) * sizeof(float);
 }
 
+// Few rows (R <= 32): the GEMM streams W once and is bound by HBM latency
+// and bandwidth.  Measured on MI355X (7B-shaped projections, R = 16), the
+// fastest plans keep about max(1024, weight bytes / 224 KB) waves in flight
+// (fewer, longer waves stream better; small matrices still need enough
+// waves to cover the chip), prefer wide column groups (an activation
+// fragment then feeds more weight tiles) and avoid cross-block split-K
+// unless K is long, where narrowing the column group would be worse.
+static void plan_few_rows(GemmShape& s, int epi_kind) {
+  const int KC = s.K / 128;
+  const int RT = round_rt(s.R);
+  const double target = std::max(1024.0, (double)s.N * s.K * 2 / (224.0 * 1024));
+  const double enough = 0.9 * target;
+  // SwiGLU pairs gate and up tiles inside a column group: NT must be even.
+  const int narrowest = epi_kind == EPI_SWIGLU ? 2 : 1;
+  for (int nt = 4; nt >= narrowest; nt /= 2) {
+    if (s.N % (16 * nt)) continue;
+    const double groups = s.N / (16 * nt);
+    int wk = 1;
+    while (wk < 8 && groups * wk < enough && KC >= 2 * wk && lds_bytes(RT, nt, 2 * wk) <= 65536) wk *= 2;
+    int S = 1;
+    if (groups * wk < enough) {
+      const bool long_k = KC >= 64;
+      if (!long_k && nt > narrowest) continue;  // short K: narrower column groups instead of split-K
+      while (S < 16 && groups * wk * S < enough && KC / (wk * S * 2) >= 3 &&
+             groups * 2 * S * s.R * nt * 16 <= (double)kGemmPartFloats && groups <= kGemmCounters)
+        S *= 2;
+    }
+    s.NT = nt;
+    s.WK = wk;
+    s.S = S;
+    // A deeper ring pays off once the grid outgrows one wave per slot.
+    s.D = (nt == 4 && groups * wk * S > 2048) ? 2 : 0;
+    return;
+  }
+}
+
 void gemm_plan(GemmShape& s, int epi_kind) {
   const int KC = s.K / 128;
   const int RT = round_rt(s.R);
-  s.NT = (epi_kind == EPI_SWIGLU) ? 2 : 1;
+  s.D = 0;
+  s.NT = 0;
+  if (RT <= 2) {
+    plan_few_rows(s, epi_kind);
+    if (s.NT > 0) return;
+  }
+  // More rows: the activation tiles dominate registers and LDS; no split-K.
+  s.NT = epi_kind == EPI_SWIGLU ? 2 : 1;
   const int groups = s.N / (16 * s.NT);
-  // Aim for >= ~2048 waves in flight (256 CUs) while keeping >= 2 K-blocks
-  // per wave, and stay inside 64 KB of LDS for the partial tiles.
   int wk = 1;
-  while (wk < 16 && groups * wk < 2048 && KC / (wk * 2) >= 2) wk *= 2;
+  while (wk < 8 && groups * wk < 2048 && KC / (wk * 2) >= 2) wk *= 2;
   while (wk > 1 && lds_bytes(RT, s.NT, wk) > 65536) wk /= 2;
   s.WK = wk;
+  s.S = 1;
 }
 
 size_t gemm_blocks(const GemmShape& s) { return (size_t)s.N / (16 * s.NT); }
 
-template <typename T, int RT, int NT, int WK>
-static hipError_t launch_t(const void* X, int ldx, const void* Wp, const GemmShape& s, const Epi& ep,
-                           hipStream_t st) {
+template <typename T, int RT, int NT, int WK, int D>
+static hipError_t launch_t(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
+                           const Epi& ep, hipStream_t st) {
   size_t lds = lds_bytes(RT, NT, WK);
-  dim3 grid((unsigned)(s.N / (16 * NT))), block(64 * WK);
-  hipLaunchKernelGGL((k_gemm<T, RT, NT, WK>), grid, block, lds, st, reinterpret_cast<const T*>(X),
-                     ldx, reinterpret_cast<const T*>(Wp), s.K / 128, ep);
+  dim3 grid((unsigned)(s.N / (16 * NT)), (unsigned)s.S), block(64 * WK);
+  hipLaunchKernelGGL((k_gemm<T, RT, NT, WK, D>), grid, block, lds, st, reinterpret_cast<const T*>(X),
+                     xplane, reinterpret_cast<const T*>(Wp), s.K / 128, pack_group(s.N), ep);
   return hipGetLastError();
 }
 
+template <typename T, int RT, int NT, int WK>
+static hipError_t launch_d(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
+                           const Epi& ep, hipStream_t st) {
+  if constexpr (NT == 4)
+    if (s.D == 2) return launch_t<T, RT, NT, WK, 2>(X, xplane, Wp, s, ep, st);
+  if (s.D != 0) return hipErrorInvalidValue;
+  return launch_t<T, RT, NT, WK, Ring<T, RT, NT, WK>::D>(X, xplane, Wp, s, ep, st);
+}
+
 template <typename T, int RT, int NT>
-static hipError_t launch_wk(const void* X, int ldx, const void* Wp, const GemmShape& s, const Epi& ep,
-                            hipStream_t st) {
+static hipError_t launch_wk(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
+                            const Epi& ep, hipStream_t st) {
   switch (s.WK) {
-    case 1: return launch_t<T, RT, NT, 1>(X, ldx, Wp, s, ep, st);
-    case 2: return launch_t<T, RT, NT, 2>(X, ldx, Wp, s, ep, st);
-    case 4: if constexpr (RT * NT <= 12) return launch_t<T, RT, NT, 4>(X, ldx, Wp, s, ep, st); break;
-    case 8: if constexpr (RT * NT <= 6) return launch_t<T, RT, NT, 8>(X, ldx, Wp, s, ep, st); break;
-    case 16: if constexpr (RT * NT <= 2) return launch_t<T, RT, NT, 16>(X, ldx, Wp, s, ep, st); break;
+    case 1: return launch_d<T, RT, NT, 1>(X, xplane, Wp, s, ep, st);
+    case 2: return launch_d<T, RT, NT, 2>(X, xplane, Wp, s, ep, st);
+    case 4: if constexpr (RT * NT <= 12) return launch_d<T, RT, NT, 4>(X, xplane, Wp, s, ep, st); break;
+    case 8: if constexpr (RT * NT <= 6) return launch_d<T, RT, NT, 8>(X, xplane, Wp, s, ep, st); break;
     default: break;
   }
   return hipErrorInvalidValue;
 }
 
 template <typename T, int RT>
-static hipError_t launch_nt(const void* X, int ldx, const void* Wp, const GemmShape& s, const Epi& ep,
-                            hipStream_t st) {
-  if (s.NT == 1) return launch_wk<T, RT, 1>(X, ldx, Wp, s, ep, st);
-  if (s.NT == 2) return launch_wk<T, RT, 2>(X, ldx, Wp, s, ep, st);
+static hipError_t launch_nt(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
+                            const Epi& ep, hipStream_t st) {
+  if (s.NT == 1) return launch_wk<T, RT, 1>(X, xplane, Wp, s, ep, st);
+  if (s.NT == 2) return launch_wk<T, RT, 2>(X, xplane, Wp, s, ep, st);
+  if constexpr (RT <= 2)
+    if (s.NT == 4) return launch_wk<T, RT, 4>(X, xplane, Wp, s, ep, st);
   return hipErrorInvalidValue;
 }
 
 template <typename T>
-static hipError_t launch_rt(const void* X, int ldx, const void* Wp, const GemmShape& s, const Epi& ep,
-                            hipStream_t st) {
+static hipError_t launch_rt(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
+                            const Epi& ep, hipStream_t st) {
   switch (round_rt(s.R)) {
-    case 1: return launch_nt<T, 1>(X, ldx, Wp, s, ep, st);
-    case 2: return launch_nt<T, 2>(X, ldx, Wp, s, ep, st);
-    case 4: return launch_nt<T, 4>(X, ldx, Wp, s, ep, st);
-    case 8: return launch_nt<T, 8>(X, ldx, Wp, s, ep, st);
-    case 12: return launch_nt<T, 12>(X, ldx, Wp, s, ep, st);
-    case 16: return launch_nt<T, 16>(X, ldx, Wp, s, ep, st);
+    case 1: return launch_nt<T, 1>(X, xplane, Wp, s, ep, st);
+    case 2: return launch_nt<T, 2>(X, xplane, Wp, s, ep, st);
+    case 4: return launch_nt<T, 4>(X, xplane, Wp, s, ep, st);
+    case 8: return launch_nt<T, 8>(X, xplane, Wp, s, ep, st);
+    case 12: return launch_nt<T, 12>(X, xplane, Wp, s, ep, st);
+    case 16: return launch_nt<T, 16>(X, xplane, Wp, s, ep, st);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_gemm(int dtype, const void* X, int ldx, const void* Wp, const GemmShape& s,
-                       const Epi& ep, hipStream_t st) {
-  if (s.R < 1 || s.R > 256 || s.K % 128 || s.N % (16 * s.NT)) return hipErrorInvalidValue;
+hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
+                       const GemmShape& s, const Epi& ep, hipStream_t st) {
+  if (s.R < 1 || s.R > 256 || s.K < 128 || s.K % 128 || s.N < 16 * s.NT || s.N % (16 * s.NT))
+    return hipErrorInvalidValue;
+  if (s.S < 1 || s.S > s.K / 128) return hipErrorInvalidValue;
+  if (s.S > 1 && (!ep.kpart || !ep.kcount || s.N / (16 * s.NT) > (int)kGemmCounters ||
+                  (size_t)(s.N / 16) * s.S * s.R * 16 > kGemmPartFloats))
+    return hipErrorInvalidValue;
   if (lds_bytes(round_rt(s.R), s.NT, s.WK) > 65536) return hipErrorInvalidValue;
-  return dtype == 1 ? launch_rt<bf16_t>(X, ldx, Wp, s, ep, st)
-                    : launch_rt<float>(X, ldx, Wp, s, ep, st);
+  return dtype == 1 ? launch_rt<bf16_t>(X, xplane, Wp, s, ep, st)
+                    : launch_rt<float>(X, xplane, Wp, s, ep, st);
 }
 
 // ---- weight packing ------------------------------------------------------------
@@ -267,14 +444,18 @@ template <typename T>
 __global__ void k_pack(int rows, int cols, const T* s0, const T* s1, const T* s2, const T* s3,
                        const int32_t* rowmap, T* dst) {
   const int KC = cols / 128;
+  const int P = pack_group(rows);
   const size_t total = (size_t)rows * cols;
   for (size_t o = (size_t)blockIdx.x * blockDim.x + threadIdx.x; o < total;
        o += (size_t)gridDim.x * blockDim.x) {
     size_t blk = o / kBlockElems;
     int r = (int)(o - blk * kBlockElems);
     int j = r >> 9, lane = (r >> 3) & 63, e = r & 7;
-    int nt = (int)(blk / KC), kc = (int)(blk - (size_t)nt * KC);
-    int row = nt * 16 + (lane & 15);
+    // blk = ((t / P) * KC + kc) * P + t % P for 16-row tile t, K-block kc
+    const size_t q = blk / P;
+    int kc = (int)(q % KC);
+    int t = (int)(q / KC) * P + (int)(blk % P);
+    int row = t * 16 + (lane & 15);
     int col = kc * 128 + 32 * (lane >> 4) + 8 * j + e;
     int src = 0, srow = row;
     if (rowmap) {

@@ -57,7 +57,7 @@ struct Layout {
   size_t page_bytes, kv_layer_bytes, kv_bytes;
   // workspace (bytes)
   size_t w_state, w_h, w_xn, w_q, w_attn, w_act, w_opart, w_ml, w_lm, w_g, w_parent, w_pos,
-      w_vis, w_cos, w_sin, w_pt, w_rowmap, w_result, ws_bytes;
+      w_vis, w_cos, w_sin, w_pt, w_rowmap, w_result, w_kpart, w_kcount, ws_bytes;
 };
 
 jf_status check_config(const jf_config* c) {
@@ -67,6 +67,7 @@ jf_status check_config(const jf_config* c) {
       c->vocab < 16)
     return fail(JF_E_SHAPE, "non-positive or too small dimension");
   if (c->d_model % 128 || c->d_ffn % 128) return fail(JF_E_SHAPE, "d_model and d_ffn must be multiples of 128");
+  if (c->d_model > 4096) return fail(JF_E_SHAPE, "d_model must be at most 4096");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
     return fail(JF_E_SHAPE, "head_dim must be 32, 64 or 128");
   if (c->n_heads % c->n_kv_heads) return fail(JF_E_SHAPE, "n_heads must be a multiple of n_kv_heads");
@@ -107,10 +108,12 @@ Layout make_layout(const jf_config& c) {
   off = 0;
   L.w_state = off; off = align_up(off + 64);
   L.w_h = off; off = align_up(off + Rp * d * 4);
-  L.w_xn = off; off = align_up(off + Rp * d * L.esz);
-  L.w_q = off; off = align_up(off + Rp * Hhd * L.esz);
-  L.w_attn = off; off = align_up(off + Rp * Hhd * L.esz);
-  L.w_act = off; off = align_up(off + Rp * F * L.esz);
+  // activations: two bf16 planes (hi, lo) for bf16 models, one fp32 plane
+  // otherwise -- 4 bytes per element either way
+  L.w_xn = off; off = align_up(off + Rp * d * 4);
+  L.w_q = off; off = align_up(off + Rp * Hhd * 4);
+  L.w_attn = off; off = align_up(off + Rp * Hhd * 4);
+  L.w_act = off; off = align_up(off + Rp * F * 4);
   L.w_opart = off; off = align_up(off + (size_t)kMaxSplits * Rp * c.n_heads * c.head_dim * 4);
   L.w_ml = off; off = align_up(off + (size_t)kMaxSplits * Rp * c.n_heads * 2 * 4);
   L.w_lm = off; off = align_up(off + (V / 16) * Rp * 8);
@@ -124,6 +127,8 @@ Layout make_layout(const jf_config& c) {
   size_t maxrows = std::max<size_t>({(size_t)L.qkv_rows, 2 * F, d, V});
   L.w_rowmap = off; off = align_up(off + maxrows * 4);
   L.w_result = off; off = align_up(off + 64);
+  L.w_kpart = off; off = align_up(off + kGemmPartFloats * 4);
+  L.w_kcount = off; off = align_up(off + kGemmCounters * 4);
   L.ws_bytes = off;
   return L;
 }
@@ -139,11 +144,20 @@ struct jf_model {
   int C_ub;          // host upper bound of the committed length
   int last_rows;     // rows of the last step (0: no step to commit)
   int last_tree;     // last step was a multi-block step
+  int prof_class = 0;                 // kernel class being timed (0: none)
+  std::vector<hipEvent_t> prof_events;  // pairs (start, end), reused
+  size_t prof_used = 0;
   int32_t* state() { return reinterpret_cast<int32_t*>(ws + L.w_state); }
   int32_t* flags() { return state() + 1; }
   template <typename P> P* at(size_t off) { return reinterpret_cast<P*>(ws + off); }
   char* layer(int l) { return packed + (size_t)l * L.layer_bytes; }
   char* kv_layer(int l) { return kv + (size_t)l * L.kv_layer_bytes; }
+  Epi epi() {
+    Epi e{};
+    e.kpart = at<float>(L.w_kpart);
+    e.kcount = at<int32_t>(L.w_kcount);
+    return e;
+  }
 };
 
 extern "C" jf_status jf_query_sizes(const jf_config* cfg, size_t* packed_bytes, size_t* kv_bytes,
@@ -238,6 +252,7 @@ extern "C" jf_status jf_model_load(const jf_config* cfg, const void* const* d_we
 
   LOAD_TRY(hipMemsetAsync(d_kv, 0, L.kv_bytes, st));
   LOAD_TRY(hipMemsetAsync(m->ws + L.w_state, 0, 64, st));
+  LOAD_TRY(hipMemsetAsync(m->ws + L.w_kcount, 0, kGemmCounters * 4, st));
   LOAD_TRY(hipMemcpyAsync(m->ws + L.w_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, st));
   LOAD_TRY(hipMemcpyAsync(m->ws + L.w_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, st));
   LOAD_TRY(hipMemcpyAsync(m->ws + L.w_pt, pt.data(), pt.size() * 4, hipMemcpyHostToDevice, st));
@@ -282,7 +297,51 @@ extern "C" jf_status jf_model_load(const jf_config* cfg, const void* const* d_we
 
 extern "C" jf_status jf_model_free(jf_model* m) {
   if (!m) return fail(JF_E_INVAL, "model is null");
+  for (hipEvent_t e : m->prof_events) (void)hipEventDestroy(e);
   delete m;
+  return JF_OK;
+}
+
+// Records an event on st if kernel class cls is being timed.
+static jf_status prof_mark(jf_model* m, int cls, hipStream_t st) {
+  if (m->prof_class != cls) return JF_OK;
+  if (m->prof_used == m->prof_events.size()) {
+    hipEvent_t e;
+    HIP_TRY(hipEventCreate(&e));
+    m->prof_events.push_back(e);
+  }
+  HIP_TRY(hipEventRecord(m->prof_events[m->prof_used++], st));
+  return JF_OK;
+}
+#define PROF(cls)                                   \
+  do {                                              \
+    jf_status ps_ = prof_mark(m, (cls), st);        \
+    if (ps_ != JF_OK) return ps_;                   \
+  } while (0)
+
+extern "C" jf_status jf_profile_begin(jf_model* m, int32_t kernel_class) {
+  if (!m) return fail(JF_E_INVAL, "model is null");
+  if (kernel_class < JF_KERNEL_QKV || kernel_class > JF_KERNEL_STEP)
+    return fail(JF_E_INVAL, "unknown kernel class %d", kernel_class);
+  m->prof_class = kernel_class;
+  m->prof_used = 0;
+  return JF_OK;
+}
+
+extern "C" jf_status jf_profile_end(jf_model* m, double* total_ms, int32_t* launches) {
+  if (!m || !total_ms || !launches) return fail(JF_E_INVAL, "null pointer argument");
+  if (m->prof_class == 0) return fail(JF_E_STATE, "no profile in progress");
+  double t = 0.0;
+  for (size_t i = 0; i + 1 < m->prof_used; i += 2) {
+    HIP_TRY(hipEventSynchronize(m->prof_events[i + 1]));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, m->prof_events[i], m->prof_events[i + 1]));
+    t += ms;
+  }
+  *total_ms = t;
+  *launches = (int32_t)(m->prof_used / 2);
+  m->prof_class = 0;
+  m->prof_used = 0;
   return JF_OK;
 }
 
@@ -303,70 +362,90 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
 
   HIP_TRY(launch_tree(sg, R, state, m->flags(), m->at<int32_t>(L.w_parent), pos,
                       m->at<uint64_t>(L.w_vis), st));
+  const size_t Rp = L.Rp;
+  const size_t pl_d = Rp * d, pl_h = Rp * Hhd, pl_f = Rp * F;  // activation plane strides
   HIP_TRY(launch_embed_norm(dt, d_tokens, R, m->packed + L.p_embed, (const float*)(m->layer(0) + L.l_an),
-                            d, c.vocab, c.rms_eps, h, xn, m->flags(), st));
-  const int splits = attn_splits(std::min(m->C_ub + R, c.max_ctx));
+                            d, c.vocab, c.rms_eps, h, xn, pl_d, m->flags(), st));
+  const int splits = attn_splits(std::min(m->C_ub + R, c.max_ctx), G,
+                                 ((H / G) * R + 15) / 16);
   for (int l = 0; l < c.n_layers; ++l) {
     char* lp = m->layer(l);
     // a3: QKV + RoPE + K/V into the cache slots C + r
     {
-      GemmShape gs{R, m->L.qkv_rows, d, 1, 1};
+      GemmShape gs{R, m->L.qkv_rows, d, 1, 1, 1};
       gemm_plan(gs, EPI_QKV);
-      Epi ep{};
+      Epi ep = m->epi();
       ep.kind = EPI_QKV; ep.R = R;
-      ep.q = m->ws + L.w_q; ep.kv = m->kv_layer(l); ep.page_table = m->at<int32_t>(L.w_pt);
+      ep.q = m->ws + L.w_q; ep.q_plane = pl_h; ep.kv = m->kv_layer(l);
+      ep.page_table = m->at<int32_t>(L.w_pt);
       ep.pos = pos; ep.state = state; ep.rope_cos = m->at<float>(L.w_cos); ep.rope_sin = m->at<float>(L.w_sin);
       ep.H = H; ep.G = G; ep.hd = hd; ep.max_ctx = c.max_ctx; ep.flags = m->flags();
-      HIP_TRY(launch_gemm(dt, xn, d, lp + L.l_qkv, gs, ep, st));
+      PROF(JF_KERNEL_QKV);
+      HIP_TRY(launch_gemm(dt, xn, pl_d, lp + L.l_qkv, gs, ep, st));
+      PROF(JF_KERNEL_QKV);
     }
     // a4: attention
     {
       AttnArgs a{};
       a.H = H; a.G = G; a.hd = hd; a.R = R; a.max_ctx = c.max_ctx; a.splits = splits;
-      a.q = m->ws + L.w_q; a.kv = m->kv_layer(l); a.page_table = m->at<int32_t>(L.w_pt);
+      a.q = m->ws + L.w_q; a.q_plane = pl_h; a.kv = m->kv_layer(l); a.page_table = m->at<int32_t>(L.w_pt);
       a.state = state; a.vis = m->at<uint64_t>(L.w_vis);
       a.o_part = m->at<float>(L.w_opart); a.ml_part = m->at<float>(L.w_ml); a.out = m->ws + L.w_attn;
+      a.out_plane = pl_h;
+      PROF(JF_KERNEL_ATTN);
       HIP_TRY(launch_attention(dt, a, st));
+      PROF(JF_KERNEL_ATTN);
     }
     // a5: O projection + residual
     {
-      GemmShape gs{R, d, Hhd, 1, 1};
+      GemmShape gs{R, d, Hhd, 1, 1, 1};
       gemm_plan(gs, EPI_RESID);
-      Epi ep{};
+      Epi ep = m->epi();
       ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
-      HIP_TRY(launch_gemm(dt, m->ws + L.w_attn, Hhd, lp + L.l_o, gs, ep, st));
+      PROF(JF_KERNEL_O);
+      HIP_TRY(launch_gemm(dt, m->ws + L.w_attn, pl_h, lp + L.l_o, gs, ep, st));
+      PROF(JF_KERNEL_O);
     }
     // a6: RMSNorm, gate/up + SwiGLU, down + residual
-    HIP_TRY(launch_rmsnorm(dt, h, d, R, (const float*)(lp + L.l_fn), d, c.rms_eps, xn, d, st));
+    HIP_TRY(launch_rmsnorm(dt, h, d, R, (const float*)(lp + L.l_fn), d, c.rms_eps, xn, pl_d, st));
     {
-      GemmShape gs{R, 2 * F, d, 2, 1};
+      GemmShape gs{R, 2 * F, d, 2, 1, 1};
       gemm_plan(gs, EPI_SWIGLU);
-      Epi ep{};
-      ep.kind = EPI_SWIGLU; ep.R = R; ep.act = m->ws + L.w_act; ep.lda = F;
-      HIP_TRY(launch_gemm(dt, xn, d, lp + L.l_gu, gs, ep, st));
+      Epi ep = m->epi();
+      ep.kind = EPI_SWIGLU; ep.R = R; ep.act = m->ws + L.w_act; ep.act_k = F; ep.act_plane = pl_f;
+      PROF(JF_KERNEL_GATEUP);
+      HIP_TRY(launch_gemm(dt, xn, pl_d, lp + L.l_gu, gs, ep, st));
+      PROF(JF_KERNEL_GATEUP);
     }
     {
-      GemmShape gs{R, d, F, 1, 1};
+      GemmShape gs{R, d, F, 1, 1, 1};
       gemm_plan(gs, EPI_RESID);
-      Epi ep{};
+      Epi ep = m->epi();
       ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
-      HIP_TRY(launch_gemm(dt, m->ws + L.w_act, F, lp + L.l_down, gs, ep, st));
+      PROF(JF_KERNEL_DOWN);
+      HIP_TRY(launch_gemm(dt, m->ws + L.w_act, pl_f, lp + L.l_down, gs, ep, st));
+      PROF(JF_KERNEL_DOWN);
     }
     const float* next_gain = l + 1 < c.n_layers ? (const float*)(m->layer(l + 1) + L.l_an)
                                                 : (const float*)(m->packed + L.p_final);
-    if (l + 1 < c.n_layers || lm != 0)
-      HIP_TRY(launch_rmsnorm(dt, h, d, R, next_gain, d, c.rms_eps, xn, d, st));
+    if (l + 1 < c.n_layers || lm == 1) {
+      HIP_TRY(launch_rmsnorm(dt, h, d, R, next_gain, d, c.rms_eps, xn, pl_d, st));
+    } else if (lm == 2) {
+      // only the last row feeds the LM head: normalise it into row 0
+      HIP_TRY(launch_rmsnorm(dt, h + (size_t)(R - 1) * d, d, 1, next_gain, d, c.rms_eps, xn, pl_d, st));
+    }
   }
   if (lm == 0) return JF_OK;
   // a7: LM head with fused argmax (logits optional)
   const int Rl = lm == 2 ? 1 : R;
-  const void* X = lm == 2 ? (const void*)(m->ws + L.w_xn + (size_t)(R - 1) * d * L.esz) : xn;
-  GemmShape gs{Rl, c.vocab, d, 1, 1};
+  GemmShape gs{Rl, c.vocab, d, 1, 1, 1};
   gemm_plan(gs, EPI_ARGMAX);
-  Epi ep{};
+  Epi ep = m->epi();
   ep.kind = EPI_ARGMAX; ep.R = Rl; ep.part = m->at<uint64_t>(L.w_lm); ep.part_stride = L.Rp;
   ep.logits = d_logits; ep.ldl = c.vocab;
-  HIP_TRY(launch_gemm(dt, X, d, m->packed + L.p_lm, gs, ep, st));
+  PROF(JF_KERNEL_LMHEAD);
+  HIP_TRY(launch_gemm(dt, xn, pl_d, m->packed + L.p_lm, gs, ep, st));
+  PROF(JF_KERNEL_LMHEAD);
   HIP_TRY(launch_argmax_reduce(ep.part, (int)gemm_blocks(gs), L.Rp, Rl, d_g, st));
   return JF_OK;
 }
@@ -425,10 +504,12 @@ extern "C" jf_status jf_jacobi_step(jf_model* m, const int32_t* d_draft, int32_t
   if (s != JF_OK) return s;
   SegArgs sg{};
   sg.n = 1; sg.first[0] = 0; sg.nrows[0] = n; sg.attach[0] = -1; sg.role[0] = 0; sg.verify_from[0] = 1;
+  PROF(JF_KERNEL_STEP);
   s = forward(m, d_draft, n, sg, 1, d_argmax, d_logits, st);
   if (s != JF_OK) return s;
   HIP_TRY(launch_accept_linear(d_draft, d_argmax, n, mode, pad_seed, m->cfg.vocab, m->state(),
                                m->flags(), reinterpret_cast<int32_t*>(d_result), d_next_draft, st));
+  PROF(JF_KERNEL_STEP);
   m->last_rows = n;
   m->last_tree = 0;
   return JF_OK;
@@ -474,10 +555,12 @@ extern "C" jf_status jf_multiblock_step(jf_model* m, const int32_t* d_tokens, in
   if (s != JF_OK) return s;
   s = check_rows(m, R, st);
   if (s != JF_OK) return s;
+  PROF(JF_KERNEL_STEP);
   s = forward(m, d_tokens, R, sg, 1, d_argmax, d_logits, st);
   if (s != JF_OK) return s;
   HIP_TRY(launch_accept_tree(sg, d_tokens, d_argmax, m->at<int32_t>(m->L.w_parent), R, m->flags(),
                              d_seg_accept, reinterpret_cast<int32_t*>(d_result), d_path, st));
+  PROF(JF_KERNEL_STEP);
   m->last_rows = R;
   m->last_tree = 1;
   return JF_OK;
@@ -556,9 +639,11 @@ extern "C" jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t h
   if (R < 1 || R > 256 || C < 0) return fail(JF_E_CAPACITY, "R must be in [1, 256] and C >= 0");
   AttnArgs a{};
   a.H = n_heads; a.G = n_kv_heads; a.hd = head_dim; a.R = R; a.max_ctx = C + R;
-  a.splits = attn_splits(C + R);
-  a.q = d_q; a.kv = d_kv_layer; a.page_table = d_page_table; a.state = nullptr; a.C_host = C;
+  a.splits = attn_splits(C + R, n_kv_heads, ((n_heads / n_kv_heads) * R + 15) / 16);
+  a.q = d_q; a.q_plane = (size_t)R * n_heads * head_dim;
+  a.kv = d_kv_layer; a.page_table = d_page_table; a.state = nullptr; a.C_host = C;
   a.vis = d_vis;
+  a.out_plane = (size_t)(R + 15) / 16 * 16 * n_heads * head_dim;  // GEMM-input layout, rows padded to 16
   a.o_part = (float*)d_ws;
   a.ml_part = (float*)((char*)d_ws + (size_t)kMaxSplits * R * n_heads * head_dim * 4);
   a.out = d_out;
@@ -597,12 +682,13 @@ extern "C" jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t 
   if (R < 1 || R > 256) return fail(JF_E_CAPACITY, "R must be in [1, 256]");
   if (d < 128 || d % 128 || V < 16 || V % 16) return fail(JF_E_SHAPE, "d multiple of 128, V multiple of 16");
   hipStream_t st = (hipStream_t)stream;
-  GemmShape gs{R, V, d, 1, 1};
+  GemmShape gs{R, V, d, 1, 1, 1};
   gemm_plan(gs, EPI_ARGMAX);
+  gs.S = 1;  // no split-K scratch in the component call
   Epi ep{};
   ep.kind = EPI_ARGMAX; ep.R = R; ep.part = (uint64_t*)d_ws; ep.part_stride = R;
   ep.logits = d_logits; ep.ldl = V;
-  HIP_TRY(launch_gemm(dtype, d_x, d, d_w_packed, gs, ep, st));
+  HIP_TRY(launch_gemm(dtype, d_x, (size_t)(R + 15) / 16 * 16 * d, d_w_packed, gs, ep, st));
   HIP_TRY(launch_argmax_reduce(ep.part, (int)gemm_blocks(gs), R, R, d_argmax, st));
   if (d_draft) {
     int32_t* zero = (int32_t*)((char*)d_ws + (size_t)(V / 16) * R * 8);

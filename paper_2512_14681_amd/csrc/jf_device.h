@@ -90,6 +90,64 @@ __device__ __forceinline__ void mfma(f32x4_t& acc, const Frag<float>& a, const F
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.w, b.hi.w, acc, 0, 0, 0);
 }
 
+// ---- activations -----------------------------------------------------------------
+// A bf16 model computes activations in fp32 and stores each one as two bf16
+// planes, hi = bf16(v) and lo = bf16(v - hi) (plane stride in elements); the
+// MFMA then runs once per plane, so the contraction sees ~16 significant bits
+// of the activation instead of 8.  An fp32 model stores one fp32 plane.
+// GEMM-input layout of an activation matrix X[R][K] (R padded to 16): 16-row
+// tiles, each a run of 128-column K-blocks; inside a 16 x 128 block element
+// (r, c) sits at j * 512 + lane * 8 + e with lane = r + 16 (c / 32),
+// j = (c % 32) / 8, e = c % 8.  That is the MFMA operand order of the packed
+// weights, so one activation fragment load is one contiguous 1 KB (bf16).
+__host__ __device__ inline size_t act_offset(int row, int col, int K) {
+  const int c = col & 127;
+  return (((size_t)(row >> 4) * (size_t)(K >> 7) + (size_t)(col >> 7)) << 11) + (size_t)((c & 31) >> 3) * 512 +
+         (size_t)((row & 15) + 16 * (c >> 5)) * 8 + (size_t)(c & 7);
+}
+
+template <typename T> struct ActFrag;
+template <> struct ActFrag<bf16_t> { Frag<bf16_t> hi, lo; };
+template <> struct ActFrag<float> { Frag<float> v; };
+
+template <typename T> __device__ __forceinline__ ActFrag<T> act_load(const T* p, size_t plane);
+template <> __device__ __forceinline__ ActFrag<bf16_t> act_load<bf16_t>(const bf16_t* p, size_t plane) {
+  ActFrag<bf16_t> a; a.hi = frag_load<bf16_t>(p); a.lo = frag_load<bf16_t>(p + plane); return a;
+}
+template <> __device__ __forceinline__ ActFrag<float> act_load<float>(const float* p, size_t plane) {
+  ActFrag<float> a; a.v = frag_load<float>(p); return a;
+}
+template <typename T> __device__ __forceinline__ ActFrag<T> act_zero();
+template <> __device__ __forceinline__ ActFrag<bf16_t> act_zero<bf16_t>() {
+  ActFrag<bf16_t> a; a.hi = frag_zero<bf16_t>(); a.lo = a.hi; return a;
+}
+template <> __device__ __forceinline__ ActFrag<float> act_zero<float>() {
+  ActFrag<float> a; a.v = frag_zero<float>(); return a;
+}
+template <typename T> __device__ __forceinline__ void act_store(T* p, size_t plane, float v);
+template <> __device__ __forceinline__ void act_store<bf16_t>(bf16_t* p, size_t plane, float v) {
+  const bf16_t hi = f32_to_bf16(v);
+  p[0] = hi;
+  p[plane] = f32_to_bf16(v - bf16_to_f32(hi));
+}
+template <> __device__ __forceinline__ void act_store<float>(float* p, size_t plane, float v) { p[0] = v; }
+
+// acc += A * B with an activation operand on either side.
+__device__ __forceinline__ void mfma(f32x4_t& acc, const ActFrag<bf16_t>& a, const Frag<bf16_t>& b) {
+  mfma(acc, a.hi, b);
+  mfma(acc, a.lo, b);
+}
+__device__ __forceinline__ void mfma(f32x4_t& acc, const ActFrag<float>& a, const Frag<float>& b) {
+  mfma(acc, a.v, b);
+}
+__device__ __forceinline__ void mfma(f32x4_t& acc, const Frag<bf16_t>& a, const ActFrag<bf16_t>& b) {
+  mfma(acc, a, b.hi);
+  mfma(acc, a, b.lo);
+}
+__device__ __forceinline__ void mfma(f32x4_t& acc, const Frag<float>& a, const ActFrag<float>& b) {
+  mfma(acc, a, b.v);
+}
+
 // ---- packed weight layout --------------------------------------------------------
 // W [N][K] (row-major, out x in) is stored as blocks of 16 rows x 128 columns.
 // Block (nt, kc) = rows 16nt.., columns 128kc.., at element offset

@@ -8,6 +8,12 @@ namespace jf {
 
 constexpr int kPage = 64;  // tokens per KV page
 
+// Packed weight layout: 16-row tiles are stored in groups of P (4 when the
+// row count allows, else 2, else 1), and inside a group K-block-major with
+// the P tiles of one K-block adjacent: block index ((t / P) * KC + kc) * P +
+// t % P for tile t and K-block kc.  A block is 16 rows x 128 inputs.
+__host__ __device__ inline int pack_group(int rows) { return rows % 64 == 0 ? 4 : (rows % 32 == 0 ? 2 : 1); }
+
 enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_QKV = 2, EPI_SWIGLU = 3, EPI_ARGMAX = 4 };
 
 // What a GEMM does with its output tile Y[R][N] (fp32 accumulators).
@@ -17,13 +23,16 @@ struct Epi {
   // EPI_STORE: f32[row * ldf + col] = y;  EPI_RESID: f32[row * ldf + col] += y
   float* f32;
   int ldf;
-  // EPI_SWIGLU: columns come in (gate tile, up tile) pairs of 16; writes
-  // act[row * lda + f] = silu(gate) * up, rounded to the element type.
+  // EPI_SWIGLU: columns come in (gate tile, up tile) pairs of 16; writes the
+  // activation act(row, f) = silu(gate) * up in the GEMM-input layout of an
+  // [R][act_k] matrix (planes act_plane apart).
   void* act;
-  int lda;
+  int act_k;
+  size_t act_plane;
   // EPI_QKV: packed rows are q heads, k heads, v heads (rope pairs (i, i+hd/2)
   // interleaved 8 by 8 inside each 16-row tile of q and k heads).
-  void* q;                   // [R][H][hd]
+  void* q;                   // [R][H][hd] activation planes, q_plane apart
+  size_t q_plane;
   void* kv;                  // this layer's pages
   const int32_t* page_table; // logical page -> physical page
   const int32_t* pos;        // [R] positions (RoPE)
@@ -38,17 +47,29 @@ struct Epi {
   int part_stride;
   float* logits;
   int ldl;
+  // Split-K across blocks (gridDim.y > 1): each block stores its partial tile
+  // in kpart; the last block of a column group (kcount) sums them in order.
+  float* kpart;
+  int32_t* kcount;
 };
 
 struct GemmShape {
   int R, N, K;   // Y[R][N] = X[R][K] * W[N][K]^T
   int NT, WK;    // 16-column tiles per block, waves splitting K per block
+  int S;         // blocks splitting K per column group
+  int D;         // register-ring depth (0: the kernel's default)
 };
 
-// Chooses NT / WK for a shape (NT fixed by the epilogue where it matters).
+// Scratch a GEMM needs for split-K partials (floats) and counters (ints).
+constexpr size_t kGemmPartFloats = (size_t)16 << 20;  // 64 MB
+constexpr size_t kGemmCounters = 16384;
+
+// Chooses NT / WK / S for a shape (NT fixed by the epilogue where it matters).
 void gemm_plan(GemmShape& s, int epi_kind);
-hipError_t launch_gemm(int dtype, const void* X, int ldx, const void* Wp, const GemmShape& s,
-                       const Epi& ep, hipStream_t stream);
+// X: activation planes of an [R][K] matrix in the GEMM-input layout
+// (act_offset; planes xplane elements apart for bf16 models).
+hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
+                       const GemmShape& s, const Epi& ep, hipStream_t stream);
 size_t gemm_blocks(const GemmShape& s);
 
 // Packs W[rows][cols] (row-major) into the kernels' block layout, reading
@@ -65,16 +86,18 @@ struct SegArgs {
 hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t* flags,
                        int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t stream);
 
+// Both write xn in the GEMM-input layout of an [R][d] matrix.
 hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int R, const void* embed,
                              const float* gamma, int d, int V, float eps, float* h, void* xn,
-                             int32_t* flags, hipStream_t stream);
+                             size_t xplane, int32_t* flags, hipStream_t stream);
 hipError_t launch_rmsnorm(int dtype, const float* h, int ldh, int R, const float* gamma, int d,
-                          float eps, void* xn, int ldx, hipStream_t stream);
+                          float eps, void* xn, size_t xplane, hipStream_t stream);
 
 struct AttnArgs {
   int H, G, hd, R, max_ctx;
   int splits;
-  const void* q;             // [R][H][hd]
+  const void* q;             // [R][H][hd] activation planes
+  size_t q_plane;
   const void* kv;            // this layer's pages
   const int32_t* page_table;
   const int32_t* state;      // state[0] = C (device), or null: use C_host
@@ -82,9 +105,10 @@ struct AttnArgs {
   const uint64_t* vis;       // [R][4] or null (causal)
   float* o_part;             // [splits][R*H][hd]
   float* ml_part;            // [splits][R*H][2]
-  void* out;                 // [R][H*hd]
+  void* out;                 // [R][H*hd] activation planes, GEMM-input layout
+  size_t out_plane;
 };
-int attn_splits(int max_keys);
+int attn_splits(int max_keys, int n_kv_heads, int n_qtiles);
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t stream);
 
 hipError_t launch_argmax_reduce(const uint64_t* part, int nblocks, int stride, int R,

@@ -61,10 +61,11 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
   return t;
 }
 
-// ---- a2 + first RMSNorm: h = E[token] (fp32), xn = round(h * rstd * gain) -------
+// ---- a2 + first RMSNorm: h = E[token] (fp32), xn = h * rstd * gain ---------------
+// xn is written in the GEMM-input layout (act_offset) of an [R][d] matrix.
 template <typename T>
 __global__ void k_embed_norm(const int32_t* tokens, const T* E, const float* gamma, int d, int V,
-                             float eps, float* h, T* xn, int32_t* flags) {
+                             float eps, float* h, T* xn, size_t xplane, int32_t* flags) {
   __shared__ float sh[16];
   const int r = blockIdx.x;
   int tok = tokens[r];
@@ -82,43 +83,55 @@ __global__ void k_embed_norm(const int32_t* tokens, const T* E, const float* gam
   ss = block_sum(ss, sh);
   const float rs = rsqrtf(ss / d + eps);
   for (int i = threadIdx.x; i < d; i += blockDim.x)
-    xn[(size_t)r * d + i] = from_f32<T>(to_f32<T>(e[i]) * rs * gamma[i]);
+    act_store<T>(xn + act_offset(r, i, d), xplane, to_f32<T>(e[i]) * rs * gamma[i]);
 }
 
 hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int R, const void* embed,
                              const float* gamma, int d, int V, float eps, float* h, void* xn,
-                             int32_t* flags, hipStream_t st) {
+                             size_t xplane, int32_t* flags, hipStream_t st) {
   if (dtype == 1)
     hipLaunchKernelGGL(k_embed_norm<bf16_t>, dim3(R), dim3(256), 0, st, tokens,
-                       (const bf16_t*)embed, gamma, d, V, eps, h, (bf16_t*)xn, flags);
+                       (const bf16_t*)embed, gamma, d, V, eps, h, (bf16_t*)xn, xplane, flags);
   else
     hipLaunchKernelGGL(k_embed_norm<float>, dim3(R), dim3(256), 0, st, tokens, (const float*)embed,
-                       gamma, d, V, eps, h, (float*)xn, flags);
+                       gamma, d, V, eps, h, (float*)xn, xplane, flags);
   return hipGetLastError();
 }
 
+// One row per block; every thread keeps its (at most 16) elements in
+// registers between the sum of squares and the scaling.
 template <typename T>
-__global__ void k_rmsnorm(const float* h, int ldh, const float* gamma, int d, float eps, T* xn,
-                          int ldx) {
+__global__ void __launch_bounds__(256) k_rmsnorm(const float* h, int ldh, const float* gamma, int d,
+                                                 float eps, T* xn, size_t xplane) {
   __shared__ float sh[16];
   const int r = blockIdx.x;
   const float* hr = h + (size_t)r * ldh;
+  float v[16];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) ss += hr[i] * hr[i];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int i = threadIdx.x + k * 256;
+    v[k] = i < d ? hr[i] : 0.f;
+    ss += v[k] * v[k];
+  }
   ss = block_sum(ss, sh);
   const float rs = rsqrtf(ss / d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x)
-    xn[(size_t)r * ldx + i] = from_f32<T>(hr[i] * rs * gamma[i]);
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int i = threadIdx.x + k * 256;
+    if (i < d) act_store<T>(xn + act_offset(r, i, d), xplane, v[k] * rs * gamma[i]);
+  }
 }
 
 hipError_t launch_rmsnorm(int dtype, const float* h, int ldh, int R, const float* gamma, int d,
-                          float eps, void* xn, int ldx, hipStream_t st) {
+                          float eps, void* xn, size_t xplane, hipStream_t st) {
+  if (d > 16 * 256) return hipErrorInvalidValue;
   if (dtype == 1)
     hipLaunchKernelGGL(k_rmsnorm<bf16_t>, dim3(R), dim3(256), 0, st, h, ldh, gamma, d, eps,
-                       (bf16_t*)xn, ldx);
+                       (bf16_t*)xn, xplane);
   else
     hipLaunchKernelGGL(k_rmsnorm<float>, dim3(R), dim3(256), 0, st, h, ldh, gamma, d, eps,
-                       (float*)xn, ldx);
+                       (float*)xn, xplane);
   return hipGetLastError();
 }
 

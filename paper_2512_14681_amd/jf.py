@@ -21,8 +21,34 @@ JF_F32, JF_BF16 = 0, 1
 JF_ROLE_RA, JF_ROLE_CAND, JF_ROLE_PSEUDO = 0, 1, 2
 JF_MAX_SEGMENTS = 16
 JF_FLAG_BAD_TOKEN, JF_FLAG_CAPACITY = 1, 2
+(JF_KERNEL_QKV, JF_KERNEL_ATTN, JF_KERNEL_O, JF_KERNEL_GATEUP, JF_KERNEL_DOWN, JF_KERNEL_LMHEAD,
+ JF_KERNEL_STEP) = range(1, 8)
 STATUS_NAMES = {0: "JF_OK", -1: "JF_E_INVAL", -2: "JF_E_SHAPE", -3: "JF_E_CAPACITY",
                 -4: "JF_E_DTYPE", -5: "JF_E_HIP", -6: "JF_E_STATE"}
+
+
+def act_layout(x):
+    """[R][K] row-major -> the GEMM-input activation layout of include/jf.h.
+
+    Rows are padded to a multiple of 16 (padding rows are zero); the result
+    is flat, ceil(R/16)*16*K elements.  K must be a multiple of 128.
+    """
+    x = np.asarray(x)
+    R, K = x.shape
+    Rp = (R + 15) // 16 * 16
+    xp = np.zeros((Rp, K), x.dtype)
+    xp[:R] = x
+    # [tile, r, kc, q, j, e] -> [tile, kc, j, q, r, e]  (lane = 16 q + r)
+    return np.ascontiguousarray(
+        xp.reshape(Rp // 16, 16, K // 128, 4, 4, 8).transpose(0, 2, 4, 3, 1, 5)).reshape(-1)
+
+
+def act_unlayout(a, R, K):
+    """Inverse of act_layout: the first R rows as an [R][K] array."""
+    a = np.asarray(a)
+    Rp = (R + 15) // 16 * 16
+    t = a[:Rp * K].reshape(Rp // 16, K // 128, 4, 4, 16, 8).transpose(0, 4, 1, 3, 2, 5)
+    return np.ascontiguousarray(t).reshape(Rp, K)[:R]
 
 
 class JfConfig(ctypes.Structure):
@@ -60,6 +86,8 @@ _SIGS = {
     "jf_kv_length": (I32, [P, ctypes.POINTER(I32), P]),
     "jf_kv_truncate": (I32, [P, I32, P]),
     "jf_kv_set_page_table": (I32, [P, ctypes.POINTER(I32), I32, P]),
+    "jf_profile_begin": (I32, [P, I32]),
+    "jf_profile_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]),
     "jf_attention_ws_bytes": (SZ, [I32, I32, I32]),
     "jf_attention": (I32, [I32, I32, I32, I32, I32, I32, P, P, P, P, P, P, P]),
     "jf_packed_matrix_bytes": (SZ, [I32, I32, I32]),
@@ -194,6 +222,14 @@ class Model:
 
     def jf_kv_truncate(self, n):
         check(lib().jf_kv_truncate(self.h, int(n), _stream(self.stream)))
+
+    def jf_profile_begin(self, kernel_class):
+        check(lib().jf_profile_begin(self.h, int(kernel_class)))
+
+    def jf_profile_end(self):
+        t, n = ctypes.c_double(), ctypes.c_int32()
+        check(lib().jf_profile_end(self.h, ctypes.byref(t), ctypes.byref(n)))
+        return t.value, n.value
 
     def jf_kv_set_page_table(self, table):
         t = np.ascontiguousarray(table, dtype=np.int32)
