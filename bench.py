@@ -24,6 +24,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "Jacobi-step latency (µs) + accepted tokens/s, 7B-shaped bf16, n=16..64, 1 GPU"
 HBM_PEAK_GBS = 8000.0
+COPY_PROBE_BYTES = 256 << 20
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_gateup_7b_n16_hbm_traffic.md")
 
 
 def log(*a):
@@ -43,6 +45,27 @@ def step_bytes(shape, n, C):
 def gateup_bytes(shape, n):
     d, F = shape["d_model"], shape["d_ffn"]
     return 2 * F * d * 2 + n * d * 2 + n * F * 2
+
+
+def measured_traffic():
+    """HBM bytes per gate/up launch from the committed hardware-counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by a copy kernel's readings),
+    or None when the summary is missing or the GEMM sources changed since
+    the counters were taken (the summary records their SHA-256)."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    fields = dict(line[2:].split(": ", 1) for line in text.splitlines()
+                  if line.startswith("- ") and ": " in line)
+    try:
+        for rel, digest in (f.split("=") for f in fields["source_sha256"].split()):
+            if hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest() != digest:
+                return None
+        return int(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError, OSError):
+        return None
 
 
 def cpu_baseline(shape, n, C, tpf, budget_s=20.0):
@@ -106,6 +129,10 @@ def main():
     ap.add_argument("--n", type=int, default=16)
     ap.add_argument("--prompt", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-profile", action="store_true",
+                    help="skip the per-kernel event pass (for hardware-counter runs)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first copy 256 MiB device-to-device 3 times (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the Jacobi step runs on a single MI355X and this "
@@ -119,6 +146,16 @@ def main():
     from paper_2512_14681_amd import decode, jf
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_probe:
+        # A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE
+        # readings give the scale from counter units to HBM bytes.
+        a = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log(f"copy probe: 3 x {COPY_PROBE_BYTES} bytes")
     shape = jf_inputs.MODEL_SHAPES["7b"]
     n, K, W = args.n, args.steps, args.warmup
     t0 = time.time()
@@ -152,13 +189,14 @@ def main():
         step(i)
     torch.cuda.synchronize()
     C0 = model.jf_kv_length()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    ev[0].record(stream)
     for i in range(W, W + K):
         step(i)
-    e1.record(stream)
+        ev[i - W + 1].record(stream)
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
+    ms = ev[0].elapsed_time(ev[K])
+    per_step_us = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)]) * 1e3
     res = d_res.cpu().numpy()
     acc = res[W:W + K, 0]
     assert (acc >= 1).all() and (res[W:W + K, 3] == 0).all(), res[W:W + K]
@@ -170,22 +208,26 @@ def main():
     # Per-kernel durations from HIP events on the library's stream, over a
     # second run of K steps (events around every launch of one class).
     kern = {}
-    for cls, name in ((jf.JF_KERNEL_GATEUP, "gateup"), (jf.JF_KERNEL_DOWN, "down"),
-                      (jf.JF_KERNEL_QKV, "qkv"), (jf.JF_KERNEL_O, "o"),
-                      (jf.JF_KERNEL_ATTN, "attn"), (jf.JF_KERNEL_LMHEAD, "lmhead")):
+    classes = () if args.no_kernel_profile else (
+        (jf.JF_KERNEL_GATEUP, "gateup"), (jf.JF_KERNEL_DOWN, "down"), (jf.JF_KERNEL_QKV, "qkv"),
+        (jf.JF_KERNEL_O, "o"), (jf.JF_KERNEL_ATTN, "attn"), (jf.JF_KERNEL_LMHEAD, "lmhead"))
+    for cls, name in classes:
         model.jf_profile_begin(cls)
         for i in range(K // 2):
             step(W + K + (i % K))
         t, cnt = model.jf_profile_end()
         kern[name] = dict(avg_us=t / cnt * 1e3, launches=cnt)
         model.jf_kv_truncate(C0 + int(acc.sum()))
+    if not kern:
+        log("per-kernel pass skipped; no roofline object")
+        return
     log("kernel averages (us): " + ", ".join(f"{k} {v['avg_us']:.1f}" for k, v in kern.items()))
     C_mid = C0 + int(acc.sum()) // 2
     gu = gateup_bytes(shape, n)
     avg_s = kern["gateup"]["avg_us"] / 1e6
     achieved = gu / avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                 "kernel": "k_gemm gate/up projection + SwiGLU (28 launches per step)",
                 "bytes_per_launch": gu, "avg_us": round(kern["gateup"]["avg_us"], 2)}
     sb = step_bytes(shape, n, C_mid)
@@ -199,6 +241,7 @@ def main():
                    "n": n, "prefix": args.prompt, "layers": shape["n_layers"],
                    "d_model": shape["d_model"], "vocab": shape["vocab"]},
         "step_us": round(ms_step * 1e3, 1), "tpf": round(tpf, 4),
+        "step_us_p10_p50_p90": [round(float(np.percentile(per_step_us, q)), 1) for q in (10, 50, 90)],
         "step_hbm_bytes": sb, "step_hbm_frac": round(sb / (ms_step / 1e3) / (HBM_PEAK_GBS * 1e9), 4),
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
         "roofline": roofline,

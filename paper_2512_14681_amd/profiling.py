@@ -1,0 +1,122 @@
+"""Summaries of rocprofv3 CSV output for libjf runs (``rocprofv3 -f csv``).
+
+    python -m paper_2512_14681_amd.profiling stats DIR
+        kernel-time table from DIR's *_kernel_stats.csv (``--kernel-trace --stats``)
+
+    python -m paper_2512_14681_amd.profiling traffic --fetch DIR1 --write DIR2 \
+        --kernel REGEX --copy-bytes N
+        HBM bytes per dispatch of the kernels matching REGEX from a FETCH_SIZE
+        run (DIR1) and a WRITE_SIZE run (DIR2).  Both counters read in KiB per
+        dispatch and are scaled by what they read for the first three dispatches
+        whose name contains "copy" (a plain device copy of N bytes that the
+        profiled program runs first, e.g. ``bench.py --copy-probe``).
+
+Both print Markdown; ``traffic`` ends with ``- key: value`` lines that
+bench.py reads back (the SHA-256 of the GEMM sources pins the figure to the
+kernel it was measured on).
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import os
+import re
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GEMM_SOURCES = ("paper_2512_14681_amd/csrc/gemm.hip", "paper_2512_14681_amd/csrc/jf_device.h",
+                "paper_2512_14681_amd/csrc/jf_internal.h")
+
+
+def _rows(directory, suffix):
+    paths = sorted(glob.glob(os.path.join(directory, "**", "*" + suffix), recursive=True))
+    if not paths:
+        raise FileNotFoundError(f"no *{suffix} under {directory}")
+    out = []
+    for p in paths:
+        with open(p, newline="") as f:
+            out.extend({k.lower(): v for k, v in r.items()} for r in csv.DictReader(f))
+    return out
+
+
+def short_name(name):
+    """'void jf::k_gemm<unsigned short, 1, 4, 2, 1>(...)' -> 'k_gemm<bf16,1,4,2,1>'."""
+    name = re.sub(r"\(.*", "", name).replace("void ", "").replace("jf::", "")
+    return name.replace("unsigned short", "bf16").replace(" ", "")
+
+
+def stats(directory, top=25):
+    rows = _rows(directory, "kernel_stats.csv")
+    total = sum(float(r["totaldurationns"]) for r in rows)
+    lines = ["| kernel | calls | avg us | total ms | % |", "|---|---:|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -float(r["totaldurationns"]))[:top]:
+        lines.append(f"| `{short_name(r['name'])[:90]}` | {int(r['calls'])} | "
+                     f"{float(r['averagens']) / 1e3:.2f} | {float(r['totaldurationns']) / 1e6:.2f} | "
+                     f"{100 * float(r['totaldurationns']) / total:.1f} |")
+    return "\n".join(lines)
+
+
+def _per_dispatch(directory, counter):
+    """[(dispatch id, kernel name, value)] of one counter, in dispatch order."""
+    out = []
+    for r in _rows(directory, "counter_collection.csv"):
+        if r.get("counter_name") == counter:
+            out.append((int(r["dispatch_id"]), r["kernel_name"], float(r["counter_value"])))
+    return sorted(out)
+
+
+def traffic(fetch_dir, write_dir, kernel_regex, copy_bytes):
+    pat = re.compile(kernel_regex)
+    res = {}
+    for label, directory, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = _per_dispatch(directory, counter)
+        copies = [v for _, k, v in rows if "copy" in k.lower()][:3]
+        if len(copies) < 3:
+            raise RuntimeError(f"{counter}: fewer than 3 copy dispatches in {directory}")
+        scale = copy_bytes / (sum(copies) / 3 * 1024)
+        vals = [v for _, k, v in rows if pat.search(k)]
+        if not vals:
+            raise RuntimeError(f"{counter}: no dispatch matches {kernel_regex!r}")
+        res[label] = dict(kib=sum(vals) / len(vals), n=len(vals), copy_kib=sum(copies) / 3, scale=scale,
+                          bytes=sum(vals) / len(vals) * 1024 * scale)
+    digests = " ".join(f"{p}={hashlib.sha256(open(os.path.join(ROOT, p), 'rb').read()).hexdigest()}"
+                       for p in GEMM_SOURCES)
+    f, w = res["fetch"], res["write"]
+    return "\n".join([
+        "| counter | dispatches | KiB per dispatch | copy probe KiB | scale (bytes per counted byte) "
+        "| HBM bytes per dispatch |",
+        "|---|---:|---:|---:|---:|---:|",
+        f"| FETCH_SIZE | {f['n']} | {f['kib']:.0f} | {f['copy_kib']:.0f} | {f['scale']:.3f} | {f['bytes']:.0f} |",
+        f"| WRITE_SIZE | {w['n']} | {w['kib']:.0f} | {w['copy_kib']:.0f} | {w['scale']:.3f} | {w['bytes']:.0f} |",
+        "",
+        f"- kernel_regex: {kernel_regex}",
+        f"- copy_probe_bytes: {copy_bytes}",
+        f"- fetch_bytes_per_launch: {f['bytes']:.0f}",
+        f"- write_bytes_per_launch: {w['bytes']:.0f}",
+        f"- hbm_bytes_per_launch: {f['bytes'] + w['bytes']:.0f}",
+        f"- source_sha256: {digests}",
+    ])
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("dir")
+    s.add_argument("--top", type=int, default=25)
+    t = sub.add_parser("traffic")
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--kernel", required=True)
+    t.add_argument("--copy-bytes", type=int, required=True)
+    a = ap.parse_args(argv)
+    if a.cmd == "stats":
+        print(stats(a.dir, a.top))
+    else:
+        print(traffic(a.fetch, a.write, a.kernel, a.copy_bytes))
+
+
+if __name__ == "__main__":
+    sys.exit(main())
