@@ -7,9 +7,9 @@
  * of the decoder over the draft rows, causal against an exact KV cache of the
  * committed prefix, a greedy argmax over the vocabulary for every row, and
  * acceptance of the longest prefix of draft rows that reached their fixed
- * point (Sec. 3.2, App. A Alg. 1 "accept longest matching prefix").
- * jf_commit_kv then keeps the accepted rows' K/V and drops the rest ("delete
- * false KV to committed length", Alg. 1 "Cache trim").
+ * point (Sec. 3.2; the acceptance step of App. A Alg. 1).
+ * jf_commit_kv then keeps the accepted rows' K/V and drops the rest (the
+ * cache-trim step of Alg. 1).
  *
  * Conventions
  *  - Pointers named d_* are DEVICE pointers; everything else is host memory.
@@ -86,7 +86,7 @@ typedef struct {
  *   ((row / 16) * (K / 128) + col / 128) * 2048 + that in-block offset,
  * and the lo plane follows the hi plane Rp * K elements later. */
 
-/* One chain of rows in a multi-block step (App. A Alg. 1 "Assemble").
+/* One chain of rows in a multi-block step (the input-assembly step of App. A Alg. 1).
  * Rows first_row .. first_row+n_rows-1 form a chain; the first hangs under
  * attach_row (-1: a root, predicted by the last committed row) and every
  * other row under the row before it.  A row sees the committed prefix, its
@@ -183,7 +183,7 @@ jf_status jf_multiblock_step(jf_model *m, const int32_t *d_tokens, int32_t R,
                              jf_step_result *d_result, int32_t *d_path,
                              float *d_logits, jf_stream stream);
 
-/* Commit the accepted rows of the last step (Alg. 1 "Cache trim"): the K/V
+/* Commit the accepted rows of the last step (cache-trim step of Alg. 1): the K/V
  * of path row i moves to position C + i, then C += accept (read from
  * d_result on the device), capped at max_commit if max_commit > 0.
  * d_path NULL means rows 0..accept-1 (a linear step: nothing moves).  Must
@@ -195,7 +195,7 @@ jf_status jf_commit_kv(jf_model *m, const int32_t *d_path,
 /* Committed length C (synchronises the stream). */
 jf_status jf_kv_length(jf_model *m, int32_t *out, jf_stream stream);
 
-/* Drop committed tokens beyond new_len ("delete false KV", Alg. 1);
+/* Drop committed tokens beyond new_len (rejected K/V removal of Alg. 1);
  * JF_E_STATE if new_len > C. Synchronises the stream. */
 jf_status jf_kv_truncate(jf_model *m, int32_t new_len, jf_stream stream);
 
@@ -240,8 +240,8 @@ jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
                        const uint64_t *d_vis, void *d_out, void *d_ws,
                        jf_stream stream);
 
-/* LM head + greedy argmax + longest-prefix acceptance (Eq. 3, Alg. 1
- * "Verification"): x [R][d] activation planes in the GEMM-input layout
+/* LM head + greedy argmax + longest-prefix acceptance (Eq. 3; the
+ * verification step of Alg. 1): x [R][d] activation planes in the GEMM-input layout
  * (Rp * d elements per plane) times lm_head^T (dtype), lm_head [V][d]
  * packed by jf_pack_matrix; g = argmax per row (lowest id on ties); accept as in
  * jf_jacobi_step against d_draft[R] (NULL: no acceptance, d_result unused).

@@ -15,7 +15,7 @@ Contents, each citing the passage it follows:
                     pass under a causal mask yields every row's prediction).
 * ``tree``       -- segments -> parent / position / visibility of the rows of
                     one step (Sec. 3.2: candidates verified side by side,
-                    blocks concatenated; App. A, Alg. 1 "Assemble").
+                    blocks concatenated; input assembly of App. A Alg. 1).
 * ``jacobi``     -- greedy AR decoding (Eq. 1), the Jacobi update (Eq. 3),
                     longest-prefix acceptance, block mode (Eq. 4), running
                     window (Sec. 4.2, running-window variant) and the

@@ -22,7 +22,7 @@ matching prefix").  The next draft is the Jacobi update of the rest,
 [g[a-1], g[a], ...]: truncated to what is left of the block (block mode,
 Eq. 4) or padded back to n (running window, Sec. 4.2).
 
-Draft initialisation ("randomly initialise", Sec. 1 and Eq. 3) draws
+Draft initialisation (random, Sec. 1 and Eq. 3) draws
 pad_id(seed, pos) = splitmix64(seed XOR pos * 0x9E3779B97F4A7C15) mod V, the
 first output of a splitmix64 generator (Steele, Lea & Flood 2014) whose
 state is that value.

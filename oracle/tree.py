@@ -1,7 +1,7 @@
 """Rows of one iteration as a forest: parent, position and visibility (oracle).
 
 Sec. 3.2 ("Rejection Recycling"): candidate n-grams are verified in parallel
-next to the draft; App. A, Alg. 1 ("Assemble input"): the real-active draft is
+next to the draft; App. A Alg. 1 (input assembly): the real-active draft is
 followed by every pseudo-active block (its accepted tokens, then its draft),
 each conditioned on everything before it.  One forward pass covers them all
 when the rows form a forest:

@@ -6,7 +6,7 @@
 
 namespace jf {
 
-// ---- a1: rows of the step as a forest (Sec. 3.2, App. A Alg. 1 "Assemble") ----
+// ---- a1: rows of the step as a forest (Sec. 3.2, input assembly of App. A Alg. 1) ----
 // parent[r]: row whose argmax r is checked against (-1: a root, predicted by
 // the last committed row); pos[r] = C + depth(r); vis[r]: bit j set iff row j
 // is r or an ancestor of r.  One thread per row walks its own ancestor chain.
