@@ -1,0 +1,183 @@
+"""GPU parity at the full 7B shape (28 layers, d 3584, 28 q / 4 kv heads of
+128, FFN 18944, vocab 152064, bf16), in the launch configurations the
+benchmark times.
+
+* Jacobi step, n = 16 running window after a 1024-token prompt (the benchmark
+  workload): all 16 rows' logits and argmaxes against the oracle.
+* Greedy Jacobi decoding with n = 16 and n = 32: every committed token is the
+  oracle's greedy prediction of its position (teacher forcing over the
+  committed sequence).
+* One multi-block step of the largest shape: a 2048-token prefix, the
+  real-active draft, 3 pseudo-active blocks and 8 candidate n-grams of 16
+  rows (R = 192) under the tree mask; one candidate holds the oracle's greedy
+  continuation and must win.
+
+The oracle runs in float32 with the bf16 K/V rounding points of the model
+(batched attention; fp32 weights cached: ~30 GB of host memory).  Bar (bf16):
+logits within 2e-2 absolute; tokens equal except where the oracle's top-2 gap
+is below 1e-3.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import jf_inputs
+from oracle import jacobi as ojac
+from oracle import tree as otree
+from oracle.model import DecoderOracle
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+SHAPE = jf_inputs.MODEL_SHAPES["7b"]
+V = SHAPE["vocab"]
+LOGIT_TOL = 2e-2
+GAP_EXEMPT = 1e-3
+
+
+def say(*a):
+    print("[7b]", *a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    from paper_2512_14681_amd import decode, jf
+    assert torch.cuda.is_available()
+    w = jf_inputs.model_weights(SHAPE, seed=0)
+    say("weights generated")
+    model = jf.Model(SHAPE, w, max_rows=256, max_ctx=2560)
+    say("model loaded")
+    ora = DecoderOracle(SHAPE, w, compute=np.float32, row_invariant=False)
+    return dict(w=w, model=model, dec=decode.Decoder(model), ora=ora, prefix=None)
+
+
+def oracle_prefix(env, prompt):
+    """The oracle's cache holds exactly `prompt`; returns its last-row logits."""
+    key = (len(prompt), hash(bytes(np.asarray(prompt, np.int64))))
+    ora = env["ora"]
+    if env["prefix"] is None or env["prefix"][0] != key:
+        ora.reset()
+        z = ora.prefill(np.asarray(prompt))
+        env["prefix"] = (key, z)
+        say(f"oracle prefill of {len(prompt)} tokens done")
+    ora.truncate(len(prompt))
+    return env["prefix"][1]
+
+
+def gap(z):
+    s = np.sort(z, axis=-1)
+    return s[..., -1] - s[..., -2]
+
+
+def teacher_forced_argmax(env, prompt, toks):
+    """The oracle's greedy prediction for every position of `toks` after `prompt`."""
+    last = oracle_prefix(env, prompt)
+    T = len(toks)
+    z, _ = env["ora"].forward(np.asarray(toks), len(prompt) + np.arange(T), np.tri(T, dtype=bool))
+    zz = np.concatenate([last[None], z[:-1]])      # row i predicts toks[i]
+    return zz.argmax(1), gap(zz)
+
+
+@pytest.fixture(scope="module")
+def prompt1024():
+    return jf_inputs.prompt(1, 1024, V)
+
+
+def test_7b_step_n16_window_logits(env, prompt1024):
+    import torch
+    dec, model = env["dec"], env["model"]
+    dec.reset()
+    p = dec.prefill(prompt1024)
+    last = oracle_prefix(env, prompt1024)
+    assert p == int(last.argmax()) or gap(last) < GAP_EXEMPT
+    n = 16
+    draft = [p] + [ojac.pad_id(2, 1024 + i, V) for i in range(1, n)]
+    d_draft = torch.tensor(draft, dtype=torch.int32, device="cuda")
+    d_next = torch.zeros(n, dtype=torch.int32, device="cuda")
+    d_log = torch.empty((n, V), dtype=torch.float32, device="cuda")
+    model.jf_jacobi_step(d_draft, n, 1, 2, dec.d_argmax, dec.d_result, d_next, d_log)
+    z = d_log.cpu().numpy()
+    g = dec.d_argmax[:n].cpu().numpy()
+    zo, _ = env["ora"].forward(np.asarray(draft), 1024 + np.arange(n), np.tri(n, dtype=bool))
+    err = np.abs(z - zo).max()
+    say(f"n=16 step: max |logit - oracle| = {err:.2e}")
+    assert err < LOGIT_TOL, err
+    assert ((g == zo.argmax(1)) | (gap(zo) < GAP_EXEMPT)).all()
+    # acceptance against the oracle's own argmax (Eq. 3 / Sec. 3.2)
+    go = zo.argmax(1)
+    a = 1
+    while a < n and draft[a] == go[a - 1]:
+        a += 1
+    res = dec.d_result.cpu().numpy()
+    if (gap(zo) >= GAP_EXEMPT).all():
+        assert res[0] == a and res[2] == go[a - 1]
+
+
+@pytest.mark.parametrize("n", [16, 32])
+def test_7b_window_decode_is_greedy(env, prompt1024, n):
+    dec = env["dec"]
+    dec.reset()
+    toks, acc = dec.generate_jacobi(prompt1024, n, 24, mode="window", pad_seed=2)
+    pred, gp = teacher_forced_argmax(env, prompt1024, toks)
+    bad = (pred != np.asarray(toks)) & (gp >= GAP_EXEMPT)
+    say(f"n={n}: {len(toks)} tokens, {len(acc)} iterations, mismatches outside near-ties: {int(bad.sum())}")
+    assert not bad.any(), np.nonzero(bad)
+    assert all(a >= 1 for a in acc)
+
+
+def test_7b_multiblock_step_r192(env):
+    """Config 5's largest step: RA (16) + 3 pseudo blocks (3 x 16) + 8 candidates (8 x 16)."""
+    import torch
+    from paper_2512_14681_amd import jf
+    dec, model, ora = env["dec"], env["model"], env["ora"]
+    prompt = jf_inputs.prompt(3, 2048, V)
+    last = oracle_prefix(env, prompt)
+    # the oracle's greedy continuation (Eq. 1), for the winning candidate
+    p = int(last.argmax())
+    ar = [p]
+    for i in range(8):
+        z, kv = ora.forward(np.asarray([ar[-1]]), np.asarray([2048 + i]), np.ones((1, 1), bool))
+        ora.commit(kv, [0])
+        ar.append(int(z[0].argmax()))
+    ora.truncate(2048)
+    say("oracle greedy continuation done")
+    n, R = 16, 192
+    segs = [(0, n, -1, jf.JF_ROLE_RA, 1)]
+    for b in range(1, 4):                                  # pseudo blocks, chained
+        segs.append((b * n, n, b * n - 1, jf.JF_ROLE_PSEUDO, 0))
+    for c in range(8):                                     # candidates under row 0
+        segs.append((64 + c * n, n, 0, jf.JF_ROLE_CAND, 0))
+    tokens = [p] + [ojac.pad_id(4, 2048 + i, V) for i in range(1, R)]
+    rng = np.random.default_rng(5)
+    for c in range(8):
+        tokens[64 + c * n:64 + (c + 1) * n] = [int(t) for t in rng.integers(0, V, n)]
+    tokens[64 + 3 * n:64 + 3 * n + 8] = ar[1:9]           # candidate 3: greedy for 8 rows
+    dec.reset()
+    gp = dec.prefill(prompt)
+    assert gp == p or gap(last) < GAP_EXEMPT
+    d_tok = torch.tensor(tokens, dtype=torch.int32, device="cuda")
+    d_arg = torch.zeros(R, dtype=torch.int32, device="cuda")
+    d_seg = torch.zeros(jf.JF_MAX_SEGMENTS, dtype=torch.int32, device="cuda")
+    d_res = torch.zeros(4, dtype=torch.int32, device="cuda")
+    d_path = torch.zeros(R, dtype=torch.int32, device="cuda")
+    d_log = torch.empty((R, V), dtype=torch.float32, device="cuda")
+    model.jf_multiblock_step(d_tok, R, segs, d_arg, d_seg, d_res, d_path, d_log)
+    z = d_log.cpu().numpy()
+    g = d_arg.cpu().numpy()
+    osegs = [otree.Segment(*s) for s in segs]
+    parent, pos, vis = otree.build(osegs, R, 2048)
+    zo, _ = ora.forward(np.asarray(tokens), pos, vis)
+    err = np.abs(z - zo).max()
+    say(f"R=192 tree step: max |logit - oracle| = {err:.2e}")
+    assert err < LOGIT_TOL, err
+    go = zo.argmax(1)
+    assert ((g == go) | (gap(zo) < GAP_EXEMPT)).all()
+    m = otree.verify(np.asarray(tokens), go, parent, osegs)
+    win, path = otree.winner_path(osegs, m, parent)
+    res = d_res.cpu().numpy()
+    if (gap(zo) >= GAP_EXEMPT).all():
+        assert list(d_seg.cpu().numpy()[:len(segs)]) == list(m)
+        assert res[1] == win and res[0] == len(path)
+        assert list(d_path.cpu().numpy()[:len(path)]) == list(path)
+    assert win == 7 and len(path) >= 9          # candidate 3 (segment 4 + 3) holds the greedy tokens
