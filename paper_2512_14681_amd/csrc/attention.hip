@@ -6,48 +6,69 @@
 //
 // Work split: block (kv head g, 16-query tile, key split).  The query rows
 // of a KV head are its n_heads/n_kv_heads query heads times R rows, 16 per
-// MFMA tile.  The block's 4 waves take interleaved 32-key chunks with the
-// next chunk's K/V loads in flight:  S^T = K Q^T (keys x queries) with K rows
-// read straight from the page, an fp32 online softmax per query column, then
-// O^T += V^T P^T with V stored transposed in the page, so both operands are
-// contiguous loads and P never leaves registers (for bf16, P is split into
-// two bf16 terms so the weights keep ~16 significant bits).  The waves' (max, sum, O)
-// states merge in LDS; a context longer than one split writes partials that
-// k_attn_combine merges.
+// MFMA tile.  The key splits are laid out over the host's upper bound of
+// C + R, so no address waits on the device's committed length (which only
+// masks), and the split's page-table entries are read once into LDS.  The
+// block's 4 waves take interleaved 32-key chunks with the next chunk's K/V
+// loads in flight: S^T = K Q^T (keys x queries), an fp32 online softmax per
+// query column, then O^T += V^T P^T.  The score tiles' rows are the chunk's
+// keys in the order 8 (i / 4) + 4 kt + i % 4, so each lane's 8 softmax
+// weights are 8 consecutive keys and its V^T operand is one contiguous load
+// from the transposed V of the page.  For bf16, Q and P enter the matrix
+// cores as two bf16 terms (hi + lo), keeping ~16 significant bits.  The
+// waves' (max, sum, O) states merge in LDS; with several splits each block
+// writes its partial state and k_attn_combine merges them in split order
+// (deterministic).
 #include "jf_device.h"
 #include "jf_internal.h"
 
 namespace jf {
 
-template <typename T> __device__ __forceinline__ Frag<T> frag_from_p(const float* p);
-template <> __device__ __forceinline__ Frag<bf16_t> frag_from_p<bf16_t>(const float* p) {
-  Frag<bf16_t> f;
-  f.v.x = (uint32_t)f32_to_bf16(p[0]) | ((uint32_t)f32_to_bf16(p[1]) << 16);
-  f.v.y = (uint32_t)f32_to_bf16(p[2]) | ((uint32_t)f32_to_bf16(p[3]) << 16);
-  f.v.z = (uint32_t)f32_to_bf16(p[4]) | ((uint32_t)f32_to_bf16(p[5]) << 16);
-  f.v.w = (uint32_t)f32_to_bf16(p[6]) | ((uint32_t)f32_to_bf16(p[7]) << 16);
+// Softmax weights as the B operand of the P.V contraction.  bf16: two terms,
+// hi = bf16(p) and lo = bf16(p - hi), so the product keeps ~16 significant
+// bits of the weights instead of 8.
+template <typename T> struct PFrag;
+template <> struct PFrag<bf16_t> { Frag<bf16_t> hi, lo; };
+template <> struct PFrag<float> { Frag<float> v; };
+
+__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  hi = pack_bf16x2(a, b);
+  lo = pack_bf16x2(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xFFFF0000u));
+}
+template <typename T> __device__ __forceinline__ PFrag<T> pfrag(const float* p);
+template <> __device__ __forceinline__ PFrag<bf16_t> pfrag<bf16_t>(const float* p) {
+  PFrag<bf16_t> f;
+  split2(p[0], p[1], f.hi.v.x, f.lo.v.x);
+  split2(p[2], p[3], f.hi.v.y, f.lo.v.y);
+  split2(p[4], p[5], f.hi.v.z, f.lo.v.z);
+  split2(p[6], p[7], f.hi.v.w, f.lo.v.w);
   return f;
 }
-template <> __device__ __forceinline__ Frag<float> frag_from_p<float>(const float* p) {
-  Frag<float> f;
-  f.lo = make_float4(p[0], p[1], p[2], p[3]);
-  f.hi = make_float4(p[4], p[5], p[6], p[7]);
+template <> __device__ __forceinline__ PFrag<float> pfrag<float>(const float* p) {
+  PFrag<float> f;
+  f.v.lo = make_float4(p[0], p[1], p[2], p[3]);
+  f.v.hi = make_float4(p[4], p[5], p[6], p[7]);
   return f;
 }
 
-// Two runs of 4 consecutive elements (the transposed-V operand).
-template <typename T> __device__ __forceinline__ Frag<T> frag_load_4x2(const T* a, const T* b);
-template <> __device__ __forceinline__ Frag<bf16_t> frag_load_4x2<bf16_t>(const bf16_t* a,
-                                                                       const bf16_t* b) {
-  uint2 x = *reinterpret_cast<const uint2*>(a), y = *reinterpret_cast<const uint2*>(b);
-  Frag<bf16_t> f; f.v = make_uint4(x.x, x.y, y.x, y.y); return f;
+constexpr int kAttnMaxPages = 256;  // pages of one key split (LDS page-table copy)
+
+// Bits j0 .. j0 + 7 of a row's 256-bit in-step visibility mask (bits outside
+// [0, 256) read as 0), branch-free.
+__device__ __forceinline__ uint32_t vis_bits8(const uint64_t (&vw)[4], int j0) {
+  const int jc = min(max(j0, 0), 255);
+  const int wi = jc >> 6, sh = jc & 63;
+  const uint64_t lo = wi == 0 ? vw[0] : (wi == 1 ? vw[1] : (wi == 2 ? vw[2] : vw[3]));
+  const uint64_t hi = wi == 0 ? vw[1] : (wi == 1 ? vw[2] : (wi == 2 ? vw[3] : 0ull));
+  const uint64_t win = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
+  uint32_t b = (uint32_t)win & 0xFFu;
+  if (j0 < 0) b = j0 > -8 ? ((uint32_t)vw[0] << (-j0)) & 0xFFu : 0u;
+  return j0 >= 256 ? 0u : b;
 }
-template <> __device__ __forceinline__ Frag<float> frag_load_4x2<float>(const float* a,
-                                                                     const float* b) {
-  Frag<float> f;
-  f.lo = *reinterpret_cast<const float4*>(a);
-  f.hi = *reinterpret_cast<const float4*>(b);
-  return f;
+
+// Low n bits set, n clamped to [0, 8].
+__device__ __forceinline__ uint32_t low_bits8(int n) {
+  return n >= 8 ? 0xFFu : (n <= 0 ? 0u : (1u << n) - 1u);
 }
 
 template <typename T, int HD>
@@ -55,20 +76,26 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   constexpr int NW = 4;  // waves per block
   __shared__ float s_m[NW][16], s_l[NW][16];
   __shared__ float s_o[NW][16][HD + 4];
+  __shared__ float s_f[NW][16], s_M[16], s_den[16];
+  __shared__ int s_pt[kAttnMaxPages];
   const int g = blockIdx.x;
   const int tile = blockIdx.y;
-  const int split = blockIdx.z;
+  const int split = blockIdx.z, S = gridDim.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = a.H / a.G;
   const int R = a.R;
   const int nq = grp * R;
-  const int C = a.state ? a.state[0] : a.C_host;
-  const int total = C + R;
-  int per = (total + a.splits - 1) / a.splits;
+  // This split's keys [k0, k1), 32-aligned, from the host's bound of C + R.
+  int per = (a.keys_ub + S - 1) / S;
   per = (per + 31) & ~31;
   const int k0 = split * per;
-  const int k1 = min(total, k0 + per);
+  const int k1 = min(a.keys_ub, k0 + per);
   const int nch = k1 > k0 ? (k1 - k0 + 31) / 32 : 0;
+  const int p0 = k0 / kPage;
+  const int np = k1 > k0 ? (k1 - 1) / kPage - p0 + 1 : 0;
+  for (int i = threadIdx.x; i < np; i += 64 * NW) s_pt[i] = a.page_table[p0 + i];
+  const int C = a.state ? a.state[0] : a.C_host;  // masks only
+  const int lim = min(k1, C + R);                 // keys at or past lim are not visible here
 
   const int ql = lane & 15, kg = lane >> 4;
   const int qr = tile * 16 + ql;
@@ -79,6 +106,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
 
   const T* kv = reinterpret_cast<const T*>(a.kv);
   const size_t page_elems = (size_t)2 * a.G * kPage * HD;
+  const size_t k_off = (size_t)g * kPage * HD;
   const size_t vt_off = (size_t)a.G * kPage * HD + (size_t)g * HD * kPage;
 
   ActFrag<T> qf[HD / 32];
@@ -96,6 +124,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
       vw[i] = r < lo ? 0ull : (r - lo >= 63 ? ~0ull : ((2ull << (r - lo)) - 1ull));
     }
   }
+  __syncthreads();  // s_pt
 
   const float scale = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
   float m_run = -INFINITY, l_run = 0.f;
@@ -103,48 +132,54 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // K rows of the two 16-key tiles and the transposed-V fragments of one
-  // 32-key chunk.
+  // One 32-key chunk (inside one page): K rows of the two score tiles, row i
+  // of tile kt being key 8 (i / 4) + 4 kt + i % 4, and the V^T fragments
+  // holding keys 8 kg .. 8 kg + 7 for dims dt * 16 + ql.
   auto load = [&](int c, Frag<T> (&kf)[2][HD / 32], Frag<T> (&vf)[HD / 16]) {
     const int kb = k0 + 32 * c;
+    const T* page = kv + (size_t)s_pt[kb / kPage - p0] * page_elems;
+    const int ko = kb % kPage;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-      int key = min(kb + kt * 16 + ql, total - 1);
-      const T* kp = kv + (size_t)a.page_table[key / kPage] * page_elems +
-                    ((size_t)g * kPage + key % kPage) * HD + 8 * kg;
+      const T* kp = page + k_off + (size_t)(ko + 8 * (ql >> 2) + 4 * kt + (ql & 3)) * HD + 8 * kg;
 #pragma unroll
       for (int cc = 0; cc < HD / 32; ++cc) kf[kt][cc] = frag_load<T>(kp + 32 * cc);
     }
-    const T* vpage = kv + (size_t)a.page_table[kb / kPage] * page_elems + vt_off + (kb % kPage);
+    const T* vp = page + vt_off + (size_t)ql * kPage + ko + 8 * kg;
 #pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) {
-      const T* vp = vpage + (size_t)(dt * 16 + ql) * kPage + 4 * kg;
-      vf[dt] = frag_load_4x2<T>(vp, vp + 16);
-    }
+    for (int dt = 0; dt < HD / 16; ++dt) vf[dt] = frag_load<T>(vp + (size_t)dt * 16 * kPage);
   };
   auto compute = [&](int c, const Frag<T> (&kf)[2][HD / 32], const Frag<T> (&vf)[HD / 16]) {
-    const int kb = k0 + 32 * c;
+    const int key0 = k0 + 32 * c + 8 * kg;  // key of p[0]; p[e] is key0 + e
     f32x4_t sc[2];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-      sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      if constexpr (sizeof(T) == 2) {
+        // Q = hi + lo: four independent accumulation chains
+        f32x4_t sh = f32x4_t{0.f, 0.f, 0.f, 0.f}, sl = sh;
 #pragma unroll
-      for (int cc = 0; cc < HD / 32; ++cc) mfma(sc[kt], kf[kt][cc], qf[cc]);
+        for (int cc = 0; cc < HD / 32; ++cc) {
+          mfma(sh, kf[kt][cc], qf[cc].hi);
+          mfma(sl, kf[kt][cc], qf[cc].lo);
+        }
+        sc[kt] = sh + sl;
+      } else {
+        sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int cc = 0; cc < HD / 32; ++cc) mfma(sc[kt], kf[kt][cc], qf[cc]);
+      }
     }
+    // visible: below lim, and either in the prefix or marked in the row's mask
+    const uint32_t vis = low_bits8(lim - key0) & (low_bits8(C - key0) | vis_bits8(vw, key0 - C));
     float p[8];
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        int key = kb + kt * 16 + 4 * kg + i;
-        bool vis = key < k1;
-        if (vis && key >= C) {
-          int j = key - C;
-          vis = (vw[j >> 6] >> (j & 63)) & 1ull;
-        }
-        float v = vis ? sc[kt][i] * scale : -INFINITY;
-        p[kt * 4 + i] = v;
+        const int e = kt * 4 + i;
+        const float v = ((vis >> e) & 1u) ? sc[kt][i] * scale : -INFINITY;
+        p[e] = v;
         mx = fmaxf(mx, v);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -153,56 +188,49 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
     // No branch: the MFMAs need every lane.  A query with nothing visible
     // yet keeps p = 0 and m = -inf.
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+    // exponents are <= 0 (or -inf): the bare hardware exp2 suffices
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
     float psum = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      p[e] = exp2f(p[e] - m_use);
+      p[e] = __builtin_amdgcn_exp2f(p[e] - m_use);
       psum += p[e];
     }
     l_run = l_run * alpha + psum;
     m_run = m_new;
-    const Frag<T> pf = frag_from_p<T>(p);
+    const PFrag<T> pf = pfrag<T>(p);
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) o[dt] *= alpha;
     if constexpr (sizeof(T) == 2) {
-      // bf16 operands: P = hi + lo with both halves bf16, so the product
-      // keeps ~16 significant bits of the softmax weights instead of 8.
-      float lo[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) lo[e] = p[e] - bf16_to_f32(f32_to_bf16(p[e]));
-      const Frag<T> pl = frag_from_p<T>(lo);
+      for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.hi);
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) {
-        o[dt] *= alpha;
-        mfma(o[dt], vf[dt], pf);
-        mfma(o[dt], vf[dt], pl);
-      }
+      for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.lo);
     } else {
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) {
-        o[dt] *= alpha;
-        mfma(o[dt], vf[dt], pf);
-      }
+      for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.v);
     }
   };
 
-  // Chunks wave, wave + NW, ... with the next chunk's K/V in flight.
+  // Chunks wave, wave + NW, ... (mine of them), two at a time: both loads
+  // are issued (unconditionally; past the end they re-read the last chunk,
+  // unused), then both chunks are consumed.  The launch plan gives each
+  // wave at most two chunks, i.e. one memory round trip.
   Frag<T> kA[2][HD / 32], kB[2][HD / 32];
   Frag<T> vA[HD / 16], vB[HD / 16];
-  int c = wave;
-  if (c < nch) load(c, kA, vA);
-  while (c < nch) {
-    if (c + NW < nch) load(c + NW, kB, vB);
-    compute(c, kA, vA);
-    c += NW;
-    if (c >= nch) break;
-    if (c + NW < nch) load(c + NW, kA, vA);
-    compute(c, kB, vB);
-    c += NW;
+  const int mine = wave < nch ? (nch - wave + NW - 1) / NW : 0;
+  for (int i = 0; i < mine; i += 2) {
+    const int cA = wave + i * NW, cB = min(cA + NW, nch - 1);
+    load(cA, kA, vA);
+    load(cB, kB, vB);
+    compute(cA, kA, vA);
+    if (i + 1 < mine) compute(cA + NW, kB, vB);
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
 
-  // Merge the waves' partial softmax states in LDS.
+  // Merge the waves' partial softmax states in LDS: per query row the
+  // waves' weights 2^(m_w - M) and the sum once, then every element.
   if (kg == 0) {
     s_m[wave][ql] = m_run;
     s_l[wave][ql] = l_run;
@@ -212,84 +240,127 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) s_o[wave][ql][dt * 16 + 4 * kg + i] = o[dt][i];
   __syncthreads();
+  if (threadIdx.x < 16) {
+    const int q = threadIdx.x;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][q]);
+    float den = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = s_m[w][q] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[w][q] - M);
+      s_f[w][q] = f;
+      den += s_l[w][q] * f;
+    }
+    s_M[q] = M;
+    s_den[q] = den;
+  }
+  __syncthreads();
   const size_t nrow = (size_t)R * a.H;
   for (int e = threadIdx.x; e < 16 * HD; e += 64 * NW) {
     const int q = e / HD, dim = e - q * HD;
     const int qq = tile * 16 + q;
     if (qq >= nq) continue;
-    float M = -INFINITY;
+    float num = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][q]);
-    float num = 0.f, den = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      if (s_m[w][q] == -INFINITY) continue;
-      const float f = exp2f(s_m[w][q] - M);
-      num += s_o[w][q][dim] * f;
-      den += s_l[w][q] * f;
-    }
+    for (int w = 0; w < NW; ++w) num += s_o[w][q][dim] * s_f[w][q];
     const int hq = qq / R, rr = qq - hq * R;
-    const size_t qidx = (size_t)rr * a.H + g * grp + hq;
-    if (a.splits == 1) {
+    if (S == 1) {
       act_store<T>(reinterpret_cast<T*>(a.out) + act_offset(rr, (g * grp + hq) * HD + dim, a.H * HD), a.out_plane,
-                   num / den);
+                   num / s_den[q]);
     } else {
+      const size_t qidx = (size_t)rr * a.H + g * grp + hq;
       a.o_part[((size_t)split * nrow + qidx) * HD + dim] = num;
       if (dim == 0) {
-        a.ml_part[((size_t)split * nrow + qidx) * 2 + 0] = M;
-        a.ml_part[((size_t)split * nrow + qidx) * 2 + 1] = den;
+        a.ml_part[((size_t)split * nrow + qidx) * 2 + 0] = s_M[q];
+        a.ml_part[((size_t)split * nrow + qidx) * 2 + 1] = s_den[q];
       }
     }
   }
 }
 
-template <typename T, int HD>
-__global__ void k_attn_combine(AttnArgs a) {
-  const size_t qidx = blockIdx.x;
-  const int dim = threadIdx.x;
-  const size_t nrow = (size_t)a.R * a.H;
-  float M = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) M = fmaxf(M, a.ml_part[((size_t)s * nrow + qidx) * 2]);
-  float num = 0.f, den = 0.f;
-  for (int s = 0; s < a.splits; ++s) {
-    float m = a.ml_part[((size_t)s * nrow + qidx) * 2];
-    if (m == -INFINITY) continue;
-    float w = exp2f(m - M);
-    num += a.o_part[((size_t)s * nrow + qidx) * HD + dim] * w;
-    den += a.ml_part[((size_t)s * nrow + qidx) * 2 + 1] * w;
+// Merges the splits' (max, sum, O) states of 16 query rows x 32 dims per
+// block in split order; every load of a thread is issued at once (SMAX >= S
+// splits unrolled, the extra ones re-reading split S - 1 with weight 0).
+template <typename T, int HD, int SMAX>
+__global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
+  const int g = blockIdx.x, tile = blockIdx.y, d0 = blockIdx.z * 32;
+  const int S = a.splits;
+  const int grp = a.H / a.G, R = a.R, nq = grp * R;
+  const size_t nrow = (size_t)R * a.H;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int e = threadIdx.x + 256 * j;
+    const int q = e >> 5, dim = d0 + (e & 31);
+    const int qq = min(tile * 16 + q, nq - 1);
+    const int hq = qq / R, rr = qq - hq * R;
+    const size_t qidx = (size_t)rr * a.H + g * grp + hq;
+    float m[SMAX], l[SMAX], ov[SMAX];
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp) {
+      const size_t i = (size_t)min(sp, S - 1) * nrow + qidx;
+      m[sp] = a.ml_part[i * 2];
+      l[sp] = a.ml_part[i * 2 + 1];
+      ov[sp] = a.o_part[i * HD + dim];
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp) M = fmaxf(M, m[sp]);
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp) {
+      const float w = (sp >= S || m[sp] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[sp] - M);
+      num += ov[sp] * w;
+      den += l[sp] * w;
+    }
+    if (tile * 16 + q < nq)
+      act_store<T>(reinterpret_cast<T*>(a.out) + act_offset(rr, (g * grp + hq) * HD + dim, a.H * HD), a.out_plane,
+                   num / den);
   }
-  const int rr = (int)(qidx / a.H), head = (int)(qidx - (size_t)rr * a.H);
-  act_store<T>(reinterpret_cast<T*>(a.out) + act_offset(rr, head * HD + dim, a.H * HD), a.out_plane, num / den);
 }
 
-// Number of key splits: enough blocks to cover the machine (>= 256 blocks
-// over kv heads x query tiles x splits), at least 128 keys per split, and at
-// most 2048 keys per split.  The split ranges are derived on the device from
-// the committed length, so any count is correct.
-int attn_splits(int max_keys, int n_kv_heads, int n_qtiles) {
-  int blocks = n_kv_heads * n_qtiles;
-  int s = (256 + blocks - 1) / blocks;
-  int by_len = max_keys / 128;
-  if (s > by_len) s = by_len;
-  int min_s = (max_keys + 2047) / 2048;
+// Launch shape: key splits such that each of a block's 4 waves gets at most
+// kAttnChunksPerWave 32-key chunks (one memory round trip), at most
+// kAttnMaxSplits splits, and at most kAttnMaxPages - 2 pages per split.
+void attn_plan(AttnArgs& a) {
+  const int chunks = (a.keys_ub + 31) / 32;
+  a.waves = 4;
+  int s = (chunks + kAttnChunksPerWave * a.waves - 1) / (kAttnChunksPerWave * a.waves);
+  const int min_s = (a.keys_ub + (kAttnMaxPages - 2) * kPage - 1) / ((kAttnMaxPages - 2) * kPage);
   if (s < min_s) s = min_s;
-  return s < 1 ? 1 : (s > 32 ? 32 : s);
+  a.splits = s < 1 ? 1 : (s > kAttnMaxSplits ? kAttnMaxSplits : s);
 }
 
 template <typename T, int HD>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const int nq = (a.H / a.G) * a.R;
   const int ntiles = (nq + 15) / 16;
-  dim3 grid(a.G, ntiles, a.splits), block(256);
-  hipLaunchKernelGGL((k_attn<T, HD>), grid, block, 0, st, a);
+  hipLaunchKernelGGL((k_attn<T, HD>), dim3(a.G, ntiles, a.splits), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(a.R * a.H), dim3(HD), 0, st, a);
+  const dim3 grid(a.G, ntiles, HD / 32);
+  if (a.splits <= 4)
+    hipLaunchKernelGGL((k_attn_combine<T, HD, 4>), grid, dim3(256), 0, st, a);
+  else if (a.splits <= 8)
+    hipLaunchKernelGGL((k_attn_combine<T, HD, 8>), grid, dim3(256), 0, st, a);
+  else if (a.splits <= 16)
+    hipLaunchKernelGGL((k_attn_combine<T, HD, 16>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_attn_combine<T, HD, 32>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
-  if (a.R < 1 || a.R > 256 || a.splits < 1 || a.H % a.G) return hipErrorInvalidValue;
+  if (a.R < 1 || a.R > 256 || a.splits < 1 || a.splits > kAttnMaxSplits || a.H % a.G || a.keys_ub < a.R ||
+      a.keys_ub > a.max_ctx)
+    return hipErrorInvalidValue;
+  // the LDS page-table copy must hold one split's pages
+  {
+    int per = (a.keys_ub + a.splits - 1) / a.splits;
+    per = (per + 31) & ~31;
+    if (per / kPage + 2 > kAttnMaxPages) return hipErrorInvalidValue;
+  }
+  if (a.splits > 1 && (!a.o_part || !a.ml_part)) return hipErrorInvalidValue;
   switch (a.hd) {
     case 32: return dtype == 1 ? launch_attn_t<bf16_t, 32>(a, st) : launch_attn_t<float, 32>(a, st);
     case 64: return dtype == 1 ? launch_attn_t<bf16_t, 64>(a, st) : launch_attn_t<float, 64>(a, st);

@@ -40,7 +40,6 @@ extern "C" const char* jf_last_error(void) { return g_err.c_str(); }
 // ---- layout ------------------------------------------------------------------------
 namespace {
 
-constexpr int kMaxSplits = 32;
 
 size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 
@@ -114,8 +113,8 @@ Layout make_layout(const jf_config& c) {
   L.w_q = off; off = align_up(off + Rp * Hhd * 4);
   L.w_attn = off; off = align_up(off + Rp * Hhd * 4);
   L.w_act = off; off = align_up(off + Rp * F * 4);
-  L.w_opart = off; off = align_up(off + (size_t)kMaxSplits * Rp * c.n_heads * c.head_dim * 4);
-  L.w_ml = off; off = align_up(off + (size_t)kMaxSplits * Rp * c.n_heads * 2 * 4);
+  L.w_opart = off; off = align_up(off + (size_t)kAttnMaxSplits * Rp * c.n_heads * c.head_dim * 4);
+  L.w_ml = off; off = align_up(off + (size_t)kAttnMaxSplits * Rp * c.n_heads * 2 * 4);
   L.w_lm = off; off = align_up(off + (V / 16) * Rp * 8);
   L.w_g = off; off = align_up(off + Rp * 4);
   L.w_parent = off; off = align_up(off + Rp * 4);
@@ -366,8 +365,7 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
   const size_t pl_d = Rp * d, pl_h = Rp * Hhd, pl_f = Rp * F;  // activation plane strides
   HIP_TRY(launch_embed_norm(dt, d_tokens, R, m->packed + L.p_embed, (const float*)(m->layer(0) + L.l_an),
                             d, c.vocab, c.rms_eps, h, xn, pl_d, m->flags(), st));
-  const int splits = attn_splits(std::min(m->C_ub + R, c.max_ctx), G,
-                                 ((H / G) * R + 15) / 16);
+  const int keys_ub = std::min(m->C_ub + R, c.max_ctx);
   for (int l = 0; l < c.n_layers; ++l) {
     char* lp = m->layer(l);
     // a3: QKV + RoPE + K/V into the cache slots C + r
@@ -387,7 +385,8 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
     // a4: attention
     {
       AttnArgs a{};
-      a.H = H; a.G = G; a.hd = hd; a.R = R; a.max_ctx = c.max_ctx; a.splits = splits;
+      a.H = H; a.G = G; a.hd = hd; a.R = R; a.max_ctx = c.max_ctx; a.keys_ub = keys_ub;
+      attn_plan(a);
       a.q = m->ws + L.w_q; a.q_plane = pl_h; a.kv = m->kv_layer(l); a.page_table = m->at<int32_t>(L.w_pt);
       a.state = state; a.vis = m->at<uint64_t>(L.w_vis);
       a.o_part = m->at<float>(L.w_opart); a.ml_part = m->at<float>(L.w_ml); a.out = m->ws + L.w_attn;
@@ -625,7 +624,8 @@ extern "C" jf_status jf_kv_set_page_table(jf_model* m, const int32_t* h_table, i
 // ---- component calls ---------------------------------------------------------------------
 extern "C" size_t jf_attention_ws_bytes(int32_t n_heads, int32_t head_dim, int32_t R) {
   if (n_heads < 1 || head_dim < 1 || R < 1) return 0;
-  return (size_t)kMaxSplits * R * n_heads * (head_dim + 2) * 4 + 256;
+  // split partials: o, then (max, sum)
+  return (size_t)kAttnMaxSplits * R * n_heads * (head_dim + 2) * 4 + 256;
 }
 
 extern "C" jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, int32_t dtype,
@@ -639,13 +639,14 @@ extern "C" jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t h
   if (R < 1 || R > 256 || C < 0) return fail(JF_E_CAPACITY, "R must be in [1, 256] and C >= 0");
   AttnArgs a{};
   a.H = n_heads; a.G = n_kv_heads; a.hd = head_dim; a.R = R; a.max_ctx = C + R;
-  a.splits = attn_splits(C + R, n_kv_heads, ((n_heads / n_kv_heads) * R + 15) / 16);
+  a.keys_ub = C + R;
+  attn_plan(a);
   a.q = d_q; a.q_plane = (size_t)R * n_heads * head_dim;
   a.kv = d_kv_layer; a.page_table = d_page_table; a.state = nullptr; a.C_host = C;
   a.vis = d_vis;
   a.out_plane = (size_t)(R + 15) / 16 * 16 * n_heads * head_dim;  // GEMM-input layout, rows padded to 16
   a.o_part = (float*)d_ws;
-  a.ml_part = (float*)((char*)d_ws + (size_t)kMaxSplits * R * n_heads * head_dim * 4);
+  a.ml_part = (float*)((char*)d_ws + (size_t)kAttnMaxSplits * R * n_heads * head_dim * 4);
   a.out = d_out;
   HIP_TRY(launch_attention(dtype, a, (hipStream_t)stream));
   return JF_OK;

@@ -93,9 +93,13 @@ hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int R, const void
 hipError_t launch_rmsnorm(int dtype, const float* h, int ldh, int R, const float* gamma, int d,
                           float eps, void* xn, size_t xplane, hipStream_t stream);
 
+constexpr int kAttnMaxSplits = 32;
+
 struct AttnArgs {
   int H, G, hd, R, max_ctx;
   int splits;
+  int waves;                 // waves per block (4)
+  int keys_ub;               // host upper bound of C + R (<= max_ctx): the split layout
   const void* q;             // [R][H][hd] activation planes
   size_t q_plane;
   const void* kv;            // this layer's pages
@@ -108,7 +112,9 @@ struct AttnArgs {
   void* out;                 // [R][H*hd] activation planes, GEMM-input layout
   size_t out_plane;
 };
-int attn_splits(int max_keys, int n_kv_heads, int n_qtiles);
+// Sets a.waves and a.splits from a.keys_ub (and the head counts).
+void attn_plan(AttnArgs& a);
+constexpr int kAttnChunksPerWave = 2;  // 32-key chunks per wave
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t stream);
 
 hipError_t launch_argmax_reduce(const uint64_t* part, int nblocks, int stride, int R,
@@ -125,6 +131,7 @@ hipError_t launch_commit(int dtype, void* kv, int L, int n_pages, int G, int hd,
                          const int32_t* result, int max_commit, int fixed_count, int max_ctx,
                          hipStream_t stream);
 hipError_t launch_set_int(int32_t* p, int32_t v, hipStream_t stream);
+hipError_t launch_fill_int(int32_t* p, int n, int32_t v, hipStream_t stream);  // p[0..n) = v
 hipError_t launch_to_f32(int dtype, const void* src, float* dst, int n, hipStream_t stream);
 hipError_t launch_copy_int(int32_t* dst, const int32_t* src, hipStream_t stream);
 

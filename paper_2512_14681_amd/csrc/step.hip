@@ -326,10 +326,19 @@ hipError_t launch_to_f32(int dtype, const void* src, float* dst, int n, hipStrea
 }
 
 __global__ void k_set_int(int32_t* p, int32_t v) { *p = v; }
+__global__ void k_fill_int(int32_t* p, int n, int32_t v) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = v;
+}
 __global__ void k_copy_int(int32_t* d, const int32_t* s) { *d = *s; }
 
 hipError_t launch_set_int(int32_t* p, int32_t v, hipStream_t st) {
   hipLaunchKernelGGL(k_set_int, dim3(1), dim3(1), 0, st, p, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_int(int32_t* p, int n, int32_t v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_int, dim3((n + 255) / 256 < 64 ? (n + 255) / 256 : 64), dim3(256), 0, st, p, n, v);
   return hipGetLastError();
 }
 hipError_t launch_copy_int(int32_t* d, const int32_t* s, hipStream_t st) {
