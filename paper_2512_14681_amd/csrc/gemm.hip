@@ -19,11 +19,30 @@ namespace jf {
 // Runs on the reduced output tile of column group ng (NT * 16 columns),
 // tile[row * tld + c], with threads tid = 0..nth-1 sharing the work.
 template <typename T>
-__device__ __forceinline__ void epilogue(const float* tile, int tld, int NT, const Epi& ep, int ng,
+__device__ __forceinline__ void epilogue(float* tile, int tld, int NT, const Epi& ep, int ng,
                                          int tid, int nth) {
   const int cols = NT * 16;
   const int R = ep.R;
-  if (ep.kind == EPI_STORE || ep.kind == EPI_RESID) {
+  if (ep.kind == EPI_RESID && ep.gain_next) {
+    // Residual add, then the next RMSNorm's input: (new h) * gain as
+    // activation planes, and the row's sum of squares over these columns.
+    T* xg = reinterpret_cast<T*>(ep.xg);
+    for (int e = tid; e < R * cols; e += nth) {
+      const int row = e / cols, c = e - row * cols;
+      const int col = ng * cols + c;
+      float* dst = ep.f32 + (size_t)row * ep.ldf + col;
+      const float hn = *dst + tile[row * tld + c];
+      *dst = hn;
+      act_store<T>(xg + act_offset(row, col, ep.ldf), ep.xg_plane, hn * ep.gain_next[col]);
+      tile[row * tld + c] = hn * hn;
+    }
+    __syncthreads();
+    for (int row = tid; row < R; row += nth) {
+      float p = 0.f;
+      for (int c = 0; c < cols; ++c) p += tile[row * tld + c];
+      ss_add(ep.ss_out, ep.ss_stride, row, p);
+    }
+  } else if (ep.kind == EPI_STORE || ep.kind == EPI_RESID) {
     for (int e = tid; e < R * cols; e += nth) {
       int row = e / cols, c = e - row * cols;
       float v = tile[row * tld + c];
@@ -137,6 +156,16 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
   const int kc1 = kb0 + ((kb1 - kb0) * (wave + 1)) / WK;
   const int nk = kc1 - kc0;
 
+  // Folded RMSNorm: the rows' fixed-point sums of squares are read now (one
+  // row per thread) and only used by the epilogue, so their latency hides
+  // behind the weight stream.
+  const bool ss_early = ep.ss_in && R <= (int)blockDim.x;
+  uint64_t ssw[3] = {0, 0, 0};
+  if (ss_early && (int)threadIdx.x < R) ss_load(ep.ss_in, ep.ss_stride, ep.row0 + threadIdx.x, ssw);
+  if (ep.ss_clear && blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < 3 * ep.ss_stride; i += blockDim.x)
+      __hip_atomic_store(ep.ss_clear + i, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
   f32x4_t acc[RT][NT];
 #pragma unroll
   for (int mt = 0; mt < RT; ++mt)
@@ -158,7 +187,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
   // Rows past R read row R-1 instead (no per-lane branch): MFMA rows are
   // independent and padding rows are never stored.
   auto xload = [&](int kc, int mt, ActFrag<T> (&x)[4]) {
-    const int row = min(mt * 16 + lrow, R - 1);
+    const int row = ep.row0 + min(mt * 16 + lrow, R - 1);
     const T* xp = X + act_offset(row, kc * 128 + koff, KC * 128);
 #pragma unroll
     for (int j = 0; j < 4; ++j) x[j] = act_load<T>(xp + j * 512, xplane);
@@ -293,6 +322,27 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
       tile[row * tld + c] = sum;
     }
     if (threadIdx.x == 0) __hip_atomic_store(ep.kcount + ng, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+  }
+  if (ep.ss_in) {
+    // Output row r times 1 / rms(h[row0 + r]): the normalisation commutes
+    // with the contraction (a per-row scale of X).
+    __shared__ float s_rs[256];
+    if (ss_early) {
+      if ((int)threadIdx.x < R) s_rs[threadIdx.x] = ss_rstd(ssw, ep.norm_inv_d, ep.norm_eps);
+    } else {
+      for (int row = threadIdx.x; row < R; row += blockDim.x) {
+        uint64_t w[3];
+        ss_load(ep.ss_in, ep.ss_stride, ep.row0 + row, w);
+        s_rs[row] = ss_rstd(w, ep.norm_inv_d, ep.norm_eps);
+      }
+    }
+    __syncthreads();
+    const int cols = NT * 16;
+    for (int e = threadIdx.x; e < R * cols; e += blockDim.x) {
+      const int row = e / cols, c = e - row * cols;
+      tile[row * tld + c] *= s_rs[row];
+    }
     __syncthreads();
   }
   epilogue<T>(tile, tld, NT, ep, ng, threadIdx.x, blockDim.x);

@@ -56,7 +56,7 @@ struct Layout {
   size_t page_bytes, kv_layer_bytes, kv_bytes;
   // workspace (bytes)
   size_t w_state, w_h, w_xn, w_q, w_attn, w_act, w_opart, w_ml, w_lm, w_g, w_parent, w_pos,
-      w_vis, w_cos, w_sin, w_pt, w_rowmap, w_result, w_kpart, w_kcount, ws_bytes;
+      w_vis, w_cos, w_sin, w_pt, w_rowmap, w_result, w_kpart, w_kcount, w_ss, ws_bytes;
 };
 
 jf_status check_config(const jf_config* c) {
@@ -128,6 +128,8 @@ Layout make_layout(const jf_config& c) {
   L.w_result = off; off = align_up(off + 64);
   L.w_kpart = off; off = align_up(off + kGemmPartFloats * 4);
   L.w_kcount = off; off = align_up(off + kGemmCounters * 4);
+  // RMSNorm sums of squares: two fixed-point accumulators of 3 word planes
+  L.w_ss = off; off = align_up(off + 2 * 3 * Rp * 8);
   L.ws_bytes = off;
   return L;
 }
@@ -363,17 +365,33 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
                       m->at<uint64_t>(L.w_vis), st));
   const size_t Rp = L.Rp;
   const size_t pl_d = Rp * d, pl_h = Rp * Hhd, pl_f = Rp * F;  // activation plane strides
-  HIP_TRY(launch_embed_norm(dt, d_tokens, R, m->packed + L.p_embed, (const float*)(m->layer(0) + L.l_an),
-                            d, c.vocab, c.rms_eps, h, xn, pl_d, m->flags(), st));
+  // The RMSNorms are folded into the projections.  Every residual add writes
+  // xn = h * (next gain) and adds the rows' sums of squares into one of two
+  // accumulators; the next projection scales its output rows by 1 / rms.
+  // ss_a feeds the QKV projections and the LM head, ss_f the gate/up ones;
+  // each producer zeroes the accumulator it does not fill (already consumed).
+  uint64_t* ss_a = m->at<uint64_t>(L.w_ss);
+  uint64_t* ss_f = ss_a + 3 * Rp;
+  const int ss_stride = (int)Rp;
+  auto norm_in = [&](Epi& ep, const uint64_t* ss) {
+    ep.ss_in = ss; ep.ss_stride = ss_stride; ep.norm_inv_d = 1.0 / d; ep.norm_eps = c.rms_eps;
+  };
+  auto norm_out = [&](Epi& ep, const float* gain, uint64_t* ss, uint64_t* clear) {
+    ep.gain_next = gain; ep.xg = xn; ep.xg_plane = pl_d; ep.ss_out = ss; ep.ss_clear = clear;
+    ep.ss_stride = ss_stride;
+  };
+  HIP_TRY(launch_embed(dt, d_tokens, R, m->packed + L.p_embed, (const float*)(m->layer(0) + L.l_an), d,
+                       c.vocab, h, xn, pl_d, ss_a, ss_f, ss_stride, m->flags(), st));
   const int keys_ub = std::min(m->C_ub + R, c.max_ctx);
   for (int l = 0; l < c.n_layers; ++l) {
     char* lp = m->layer(l);
-    // a3: QKV + RoPE + K/V into the cache slots C + r
+    // a3: attention RMSNorm (folded) + QKV + RoPE + K/V into the cache slots C + r
     {
       GemmShape gs{R, m->L.qkv_rows, d, 1, 1, 1};
       gemm_plan(gs, EPI_QKV);
       Epi ep = m->epi();
       ep.kind = EPI_QKV; ep.R = R;
+      norm_in(ep, ss_a);
       ep.q = m->ws + L.w_q; ep.q_plane = pl_h; ep.kv = m->kv_layer(l);
       ep.page_table = m->at<int32_t>(L.w_pt);
       ep.pos = pos; ep.state = state; ep.rope_cos = m->at<float>(L.w_cos); ep.rope_sin = m->at<float>(L.w_sin);
@@ -395,53 +413,55 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
       HIP_TRY(launch_attention(dt, a, st));
       PROF(JF_KERNEL_ATTN);
     }
-    // a5: O projection + residual
+    // a5: O projection + residual, writing the FFN RMSNorm's input
     {
       GemmShape gs{R, d, Hhd, 1, 1, 1};
       gemm_plan(gs, EPI_RESID);
       Epi ep = m->epi();
       ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
+      norm_out(ep, (const float*)(lp + L.l_fn), ss_f, ss_a);
       PROF(JF_KERNEL_O);
       HIP_TRY(launch_gemm(dt, m->ws + L.w_attn, pl_h, lp + L.l_o, gs, ep, st));
       PROF(JF_KERNEL_O);
     }
-    // a6: RMSNorm, gate/up + SwiGLU, down + residual
-    HIP_TRY(launch_rmsnorm(dt, h, d, R, (const float*)(lp + L.l_fn), d, c.rms_eps, xn, pl_d, st));
+    // a6: FFN RMSNorm (folded), gate/up + SwiGLU, down + residual
     {
       GemmShape gs{R, 2 * F, d, 2, 1, 1};
       gemm_plan(gs, EPI_SWIGLU);
       Epi ep = m->epi();
       ep.kind = EPI_SWIGLU; ep.R = R; ep.act = m->ws + L.w_act; ep.act_k = F; ep.act_plane = pl_f;
+      norm_in(ep, ss_f);
       PROF(JF_KERNEL_GATEUP);
       HIP_TRY(launch_gemm(dt, xn, pl_d, lp + L.l_gu, gs, ep, st));
       PROF(JF_KERNEL_GATEUP);
     }
+    // down projection + residual, writing the next RMSNorm's input (the next
+    // layer's attention norm, or the final norm before the LM head)
     {
       GemmShape gs{R, d, F, 1, 1, 1};
       gemm_plan(gs, EPI_RESID);
       Epi ep = m->epi();
       ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
+      if (l + 1 < c.n_layers)
+        norm_out(ep, (const float*)(m->layer(l + 1) + L.l_an), ss_a, ss_f);
+      else if (lm != 0)
+        norm_out(ep, (const float*)(m->packed + L.p_final), ss_a, ss_f);
       PROF(JF_KERNEL_DOWN);
       HIP_TRY(launch_gemm(dt, m->ws + L.w_act, pl_f, lp + L.l_down, gs, ep, st));
       PROF(JF_KERNEL_DOWN);
     }
-    const float* next_gain = l + 1 < c.n_layers ? (const float*)(m->layer(l + 1) + L.l_an)
-                                                : (const float*)(m->packed + L.p_final);
-    if (l + 1 < c.n_layers || lm == 1) {
-      HIP_TRY(launch_rmsnorm(dt, h, d, R, next_gain, d, c.rms_eps, xn, pl_d, st));
-    } else if (lm == 2) {
-      // only the last row feeds the LM head: normalise it into row 0
-      HIP_TRY(launch_rmsnorm(dt, h + (size_t)(R - 1) * d, d, 1, next_gain, d, c.rms_eps, xn, pl_d, st));
-    }
   }
   if (lm == 0) return JF_OK;
-  // a7: LM head with fused argmax (logits optional)
+  // a7: final RMSNorm (folded) + LM head with fused argmax (logits optional);
+  // lm == 2 reads only the last row
   const int Rl = lm == 2 ? 1 : R;
   GemmShape gs{Rl, c.vocab, d, 1, 1, 1};
   gemm_plan(gs, EPI_ARGMAX);
   Epi ep = m->epi();
   ep.kind = EPI_ARGMAX; ep.R = Rl; ep.part = m->at<uint64_t>(L.w_lm); ep.part_stride = L.Rp;
   ep.logits = d_logits; ep.ldl = c.vocab;
+  ep.row0 = lm == 2 ? R - 1 : 0;
+  norm_in(ep, ss_a);
   PROF(JF_KERNEL_LMHEAD);
   HIP_TRY(launch_gemm(dt, xn, pl_d, m->packed + L.p_lm, gs, ep, st));
   PROF(JF_KERNEL_LMHEAD);

@@ -173,6 +173,42 @@ __device__ __forceinline__ uint32_t argmax_key_index(uint64_t k) {
   return 0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFull);
 }
 
+// ---- RMSNorm row statistics ------------------------------------------------------
+// Sums of squares of a row are accumulated across blocks as exact fixed-point
+// words: a non-negative fp32 partial p is split into w0 = floor(p) and two
+// 32-bit fraction words (p = w0 + w1 2^-32 + w2 2^-64, exact for p >= 2^-40;
+// below that the tail is truncated).  Each word is added to its own 64-bit
+// accumulator, so the total is the same whatever order the blocks arrive in
+// (integer addition is associative) and no carry crosses words while adding.
+// An accumulator of R rows is three word planes of `stride` entries.
+__device__ __forceinline__ void ss_split(float p, uint64_t (&w)[3]) {
+  double d = p < 1e18f ? (double)p : 1e18;  // non-finite or absurd partials saturate
+  const double w0 = floor(d);
+  d = (d - w0) * 4294967296.0;
+  const double w1 = floor(d);
+  d = (d - w1) * 4294967296.0;
+  w[0] = (uint64_t)w0;
+  w[1] = (uint64_t)w1;
+  w[2] = (uint64_t)floor(d);
+}
+__device__ __forceinline__ void ss_add(uint64_t* acc, int stride, int row, float p) {
+  uint64_t w[3];
+  ss_split(p, w);
+#pragma unroll
+  for (int k = 0; k < 3; ++k)
+    if (w[k]) __hip_atomic_fetch_add(acc + (size_t)k * stride + row, w[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void ss_load(const uint64_t* acc, int stride, int row, uint64_t (&w)[3]) {
+#pragma unroll
+  for (int k = 0; k < 3; ++k)
+    w[k] = __hip_atomic_load(acc + (size_t)k * stride + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// 1 / sqrt(mean of squares + eps) of a row from its accumulated words.
+__device__ __forceinline__ float ss_rstd(const uint64_t (&w)[3], double inv_d, double eps) {
+  const double ss = (double)w[0] + (double)w[1] * 0x1p-32 + (double)w[2] * 0x1p-64;
+  return (float)(1.0 / sqrt(ss * inv_d + eps));
+}
+
 // splitmix64 (Steele, Lea & Flood 2014): first output of the generator whose
 // state is x.
 __device__ __forceinline__ uint64_t splitmix64(uint64_t x) {

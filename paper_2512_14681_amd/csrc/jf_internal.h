@@ -51,6 +51,26 @@ struct Epi {
   // in kpart; the last block of a column group (kcount) sums them in order.
   float* kpart;
   int32_t* kcount;
+  // Input rows row0 .. row0 + R - 1 of X are read (the LM head of a prefill
+  // chunk reads only its last row).
+  int row0;
+  // RMSNorm folded into the consumer: X holds activation planes of h * gain
+  // and output row r is scaled by 1 / sqrt(mean(h[row0 + r]^2) + eps), read
+  // from ss_in, the fixed-point sums of squares of h (ss_add; three word
+  // planes of ss_stride entries).  Null: no scaling.
+  const uint64_t* ss_in;
+  int ss_stride;
+  double norm_inv_d, norm_eps;
+  // RMSNorm producer side (EPI_RESID): after f32 += y, also writes activation
+  // planes of (new h) * gain_next into xg (GEMM-input layout of an [R][ldf]
+  // matrix, planes xg_plane apart) and adds each row's sum of squares over
+  // this block's columns to ss_out.  ss_clear (may be null) is zeroed by the
+  // first block: the other accumulator, which the next producer fills.
+  const float* gain_next;
+  void* xg;
+  size_t xg_plane;
+  uint64_t* ss_out;
+  uint64_t* ss_clear;
 };
 
 struct GemmShape {
@@ -86,12 +106,14 @@ struct SegArgs {
 hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t* flags,
                        int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t stream);
 
-// Both write xn in the GEMM-input layout of an [R][d] matrix.
-hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int R, const void* embed,
-                             const float* gamma, int d, int V, float eps, float* h, void* xn,
-                             size_t xplane, int32_t* flags, hipStream_t stream);
-hipError_t launch_rmsnorm(int dtype, const float* h, int ldh, int R, const float* gamma, int d,
-                          float eps, void* xn, size_t xplane, hipStream_t stream);
+// Embedding rows h[r] = E[token r] (fp32, row-major [R][d]) with the first
+// RMSNorm's input: activation planes of h * gamma in the GEMM-input layout
+// (xg) and each row's sum of squares stored into the fixed-point accumulator
+// ss (three word planes of ss_stride entries); ss_clear is zeroed.
+hipError_t launch_embed(int dtype, const int32_t* tokens, int R, const void* embed,
+                        const float* gamma, int d, int V, float* h, void* xg, size_t xplane,
+                        uint64_t* ss, uint64_t* ss_clear, int ss_stride, int32_t* flags,
+                        hipStream_t stream);
 
 constexpr int kAttnMaxSplits = 32;
 

@@ -1,6 +1,8 @@
 // The non-GEMM kernels of one Jacobi iteration: the row forest of the step,
-// embedding + RMSNorm, RMSNorm, the vocabulary argmax reduction, greedy
-// acceptance and the KV commit.
+// the embedding gather, the vocabulary argmax reduction, greedy acceptance
+// and the KV commit.  (The RMSNorms are folded into the projections: the
+// residual adds write h * gain and the row sums of squares, the consumer
+// GEMMs scale their output rows by 1 / rms.)
 #include "jf_device.h"
 #include "jf_internal.h"
 
@@ -61,77 +63,66 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
   return t;
 }
 
-// ---- a2 + first RMSNorm: h = E[token] (fp32), xn = h * rstd * gain ---------------
-// xn is written in the GEMM-input layout (act_offset) of an [R][d] matrix.
+// ---- a2: embedding rows + the first RMSNorm's input -------------------------------
+// h = E[token] (fp32); xg = h * gamma as activation planes in the GEMM-input
+// layout; the row's sum of squares goes to the fixed-point accumulator ss
+// (the QKV projection applies 1 / rms to its output rows).  Block 0 also
+// zeroes ss_clear, the accumulator the first residual add fills.
 template <typename T>
-__global__ void k_embed_norm(const int32_t* tokens, const T* E, const float* gamma, int d, int V,
-                             float eps, float* h, T* xn, size_t xplane, int32_t* flags) {
+__global__ void __launch_bounds__(256)
+    k_embed(const int32_t* __restrict__ tokens, const T* __restrict__ E, const float* __restrict__ gamma, int d,
+            int V, float* __restrict__ h, T* __restrict__ xg, size_t xplane, uint64_t* ss, uint64_t* ss_clear,
+            int ss_stride, int32_t* flags) {
   __shared__ float sh[16];
   const int r = blockIdx.x;
+  if (r == 0 && ss_clear)
+    for (int i = threadIdx.x; i < 3 * ss_stride; i += blockDim.x)
+      __hip_atomic_store(ss_clear + i, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   int tok = tokens[r];
   if (tok < 0 || tok >= V) {
     if (threadIdx.x == 0 && flags) atomicOr(flags, 1);
     tok = 0;
   }
   const T* e = E + (size_t)tok * d;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    float v = to_f32<T>(e[i]);
-    h[(size_t)r * d + i] = v;
-    ss += v * v;
-  }
-  ss = block_sum(ss, sh);
-  const float rs = rsqrtf(ss / d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x)
-    act_store<T>(xn + act_offset(r, i, d), xplane, to_f32<T>(e[i]) * rs * gamma[i]);
-}
-
-hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int R, const void* embed,
-                             const float* gamma, int d, int V, float eps, float* h, void* xn,
-                             size_t xplane, int32_t* flags, hipStream_t st) {
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_embed_norm<bf16_t>, dim3(R), dim3(256), 0, st, tokens,
-                       (const bf16_t*)embed, gamma, d, V, eps, h, (bf16_t*)xn, xplane, flags);
-  else
-    hipLaunchKernelGGL(k_embed_norm<float>, dim3(R), dim3(256), 0, st, tokens, (const float*)embed,
-                       gamma, d, V, eps, h, (float*)xn, xplane, flags);
-  return hipGetLastError();
-}
-
-// One row per block; every thread keeps its (at most 16) elements in
-// registers between the sum of squares and the scaling.
-template <typename T>
-__global__ void __launch_bounds__(256) k_rmsnorm(const float* h, int ldh, const float* gamma, int d,
-                                                 float eps, T* xn, size_t xplane) {
-  __shared__ float sh[16];
-  const int r = blockIdx.x;
-  const float* hr = h + (size_t)r * ldh;
-  float v[16];
-  float ss = 0.f;
+  // d <= 4096: every thread's (at most 16) elements and gains are loaded at
+  // once, then stored.
+  float v[16], gm[16];
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    const int i = threadIdx.x + k * 256;
-    v[k] = i < d ? hr[i] : 0.f;
-    ss += v[k] * v[k];
+    const int i = threadIdx.x + 256 * k;
+    v[k] = i < d ? to_f32<T>(e[i]) : 0.f;
+    gm[k] = i < d ? gamma[i] : 0.f;
   }
-  ss = block_sum(ss, sh);
-  const float rs = rsqrtf(ss / d + eps);
+  float ss_part = 0.f;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    const int i = threadIdx.x + k * 256;
-    if (i < d) act_store<T>(xn + act_offset(r, i, d), xplane, v[k] * rs * gamma[i]);
+    const int i = threadIdx.x + 256 * k;
+    if (i < d) {
+      h[(size_t)r * d + i] = v[k];
+      act_store<T>(xg + act_offset(r, i, d), xplane, v[k] * gm[k]);
+    }
+    ss_part += v[k] * v[k];
+  }
+  const float tot = block_sum(ss_part, sh);
+  if (threadIdx.x == 0) {
+    uint64_t w[3];
+    ss_split(tot, w);
+    for (int k = 0; k < 3; ++k)
+      __hip_atomic_store(ss + (size_t)k * ss_stride + r, w[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
-hipError_t launch_rmsnorm(int dtype, const float* h, int ldh, int R, const float* gamma, int d,
-                          float eps, void* xn, size_t xplane, hipStream_t st) {
-  if (d > 16 * 256) return hipErrorInvalidValue;
+hipError_t launch_embed(int dtype, const int32_t* tokens, int R, const void* embed,
+                        const float* gamma, int d, int V, float* h, void* xg, size_t xplane,
+                        uint64_t* ss, uint64_t* ss_clear, int ss_stride, int32_t* flags,
+                        hipStream_t st) {
+  if (R < 1 || R > ss_stride || d > 16 * 256) return hipErrorInvalidValue;
   if (dtype == 1)
-    hipLaunchKernelGGL(k_rmsnorm<bf16_t>, dim3(R), dim3(256), 0, st, h, ldh, gamma, d, eps,
-                       (bf16_t*)xn, xplane);
+    hipLaunchKernelGGL(k_embed<bf16_t>, dim3(R), dim3(256), 0, st, tokens, (const bf16_t*)embed, gamma,
+                       d, V, h, (bf16_t*)xg, xplane, ss, ss_clear, ss_stride, flags);
   else
-    hipLaunchKernelGGL(k_rmsnorm<float>, dim3(R), dim3(256), 0, st, h, ldh, gamma, d, eps,
-                       (float*)xn, xplane);
+    hipLaunchKernelGGL(k_embed<float>, dim3(R), dim3(256), 0, st, tokens, (const float*)embed, gamma, d,
+                       V, h, (float*)xg, xplane, ss, ss_clear, ss_stride, flags);
   return hipGetLastError();
 }
 
