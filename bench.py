@@ -121,6 +121,227 @@ def cpu_baseline(shape, n, C, tpf, budget_s=20.0):
             "s_per_step": t, "affinity_cores": len(os.sched_getaffinity(0))}
 
 
+
+def _bits(t):
+    """A torch bf16 tensor's bit patterns as int16 (the ABI's bf16 storage)."""
+    return t.contiguous().view(__import__("torch").int16)
+
+
+def _time_calls(fn, iters, stream):
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(iters):
+        fn(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / iters * 1e3  # us per call
+
+
+def bench_attention(sets=32):
+    """Attention workload: 28 q / 4 KV heads of 128, N(0,1) bf16 Q/K/V, prefix
+    P, n draft queries causal within the block.  Each call reads a different
+    one of `sets` buffer sets (> 256 MB in total for P = 8192), so the K/V
+    come from HBM as in a decode step, not from the last-level cache."""
+    import torch
+    from paper_2512_14681_amd import jf
+    L = jf.lib()
+    H, G, hd = 28, 4, 128
+    st = torch.cuda.current_stream()
+    g = torch.Generator(device="cuda")
+    out = []
+    for P in (512, 2048, 8192):
+        for n in (16, 32, 64):
+            g.manual_seed(10 + P + n)
+            keys = P + n
+            pages = (keys + 63) // 64
+            page_elems = 2 * G * 64 * hd
+            kv = torch.randn(sets, pages * page_elems, device="cuda", generator=g).to(torch.bfloat16)
+            q = torch.randn(sets, 2, n * H * hd, device="cuda", generator=g).to(torch.bfloat16)
+            q[:, 1].zero_()                      # lo plane of a bf16 activation: exact
+            pt = torch.arange(pages, dtype=torch.int32, device="cuda")
+            Rp = (n + 15) // 16 * 16
+            o = torch.empty(2, Rp * H * hd, dtype=torch.int16, device="cuda")
+            ws = torch.empty(L.jf_attention_ws_bytes(H, hd, n), dtype=torch.uint8, device="cuda")
+            kvb, qb = _bits(kv), _bits(q)
+
+            def call(i):
+                jf.check(L.jf_attention(H, G, hd, jf.JF_BF16, P, n, jf._ptr(qb[i % sets]), jf._ptr(kvb[i % sets]),
+                                        jf._ptr(pt), None, jf._ptr(o), jf._ptr(ws), jf._stream(st)))
+            for i in range(4):
+                call(i)
+            us = _time_calls(call, 2 * sets, st)
+            nbytes = keys * G * hd * 2 * 2 + n * H * hd * 2 + n * H * hd * 4
+            flops = 4 * H * hd * (n * P + n * (n + 1) // 2)
+            out.append({"P": P, "n": n, "us": round(us, 2), "GB_s": round(nbytes / us / 1e3, 1),
+                        "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
+                        "TFLOP_s": round(flops / us / 1e6, 2)})
+            del kv, q, kvb, qb
+    log("attention: " + ", ".join(f"P{r['P']}/n{r['n']} {r['us']}us" for r in out))
+    return {"workload": "attention, 28 q / 4 kv heads x 128, bf16, prefix P + n causal draft rows, "
+                        f"{sets} rotating buffer sets", "calls": out}
+
+
+def bench_lm_head(trials=100):
+    """LM head + acceptance: hidden [64, 3584] N(0,1), W [152064, 3584]
+    N(0,0.02) bf16; per-row argmax, then the longest prefix with
+    draft[i] == argmax[i-1], drafts = the shifted argmax perturbed at one
+    random position p per trial (accept must equal p)."""
+    import numpy as np
+    import torch
+    from paper_2512_14681_amd import jf
+    L = jf.lib()
+    R, d, V = 64, 3584, 152064
+    st = torch.cuda.current_stream()
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1000)
+    w = torch.randn(V, d, device="cuda", generator=g).mul_(0.02).to(torch.bfloat16)
+    wp = torch.empty(L.jf_packed_matrix_bytes(V, d, jf.JF_BF16), dtype=torch.uint8, device="cuda")
+    jf.check(L.jf_pack_matrix(V, d, jf.JF_BF16, jf._ptr(_bits(w)), jf._ptr(wp), jf._stream(st)))
+    del w
+    x = torch.randn(R, d, device="cuda", generator=g).to(torch.bfloat16)
+    # GEMM-input layout of include/jf.h: hi plane = the bf16 values, lo plane = 0
+    xl = x.view(torch.int16).reshape(R // 16, 16, d // 128, 4, 4, 8).permute(0, 2, 4, 3, 1, 5).reshape(-1)
+    xp = torch.zeros(2, R * d, dtype=torch.int16, device="cuda")
+    xp[0].copy_(xl)
+    am = torch.zeros(R, dtype=torch.int32, device="cuda")
+    res = torch.zeros(trials, 4, dtype=torch.int32, device="cuda")
+    ws = torch.empty(L.jf_lm_head_ws_bytes(R, V), dtype=torch.uint8, device="cuda")
+    jf.check(L.jf_lm_head_accept(R, d, V, jf.JF_BF16, jf._ptr(xp), jf._ptr(wp), None, jf._ptr(am), None, None,
+                                 jf._ptr(ws), jf._stream(st)))
+    g0 = am.cpu().numpy()
+    rng = np.random.default_rng(1000)
+    ps = rng.integers(1, R, trials)
+    drafts = np.zeros((trials, R), np.int32)
+    for t, pp in enumerate(ps):
+        dr = np.concatenate([[5], g0[:-1]]).astype(np.int32)
+        dr[pp] = (dr[pp] + 1) % V
+        drafts[t] = dr
+    d_dr = torch.as_tensor(drafts, device="cuda")
+
+    def call(i):
+        jf.check(L.jf_lm_head_accept(R, d, V, jf.JF_BF16, jf._ptr(xp), jf._ptr(wp), jf._ptr(d_dr[i]), jf._ptr(am),
+                                     jf._ptr(res[i]), None, jf._ptr(ws), jf._stream(st)))
+    us = _time_calls(call, trials, st)
+    acc = res[:, 0].cpu().numpy()
+    nbytes = V * d * 2 + R * d * 4
+    out = {"workload": "LM head + acceptance, hidden [64, 3584], W [152064, 3584] bf16, "
+                       f"{trials} trials", "us": round(us, 2), "GB_s": round(nbytes / us / 1e3, 1),
+           "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
+           "accept_equals_p": bool((acc == ps).all())}
+    log(f"lm head + acceptance: {us:.1f} us, accept == p in all trials: {out['accept_equals_p']}")
+    return out
+
+
+def bench_tiny():
+    """Tiny fp32 decoder (2 layers, d 128, vocab 1024): 32-token prompt, block
+    Jacobi decoding with n = 8, 64 new tokens (wall clock per iteration,
+    including the per-iteration result read)."""
+    import jf_inputs
+    from paper_2512_14681_amd import decode, jf
+    shape = jf_inputs.MODEL_SHAPES["tiny"]
+    model = jf.Model(shape, jf_inputs.model_weights(shape, seed=0), max_rows=16, max_ctx=128)
+    dec = decode.Decoder(model)
+    prompt = jf_inputs.prompt(1, 32, shape["vocab"])
+    dec.generate_jacobi(prompt, 8, 64, mode="block", pad_seed=2)      # warm-up
+    dec.reset()
+    t0 = time.perf_counter()
+    toks, acc = dec.generate_jacobi(prompt, 8, 64, mode="block", pad_seed=2)
+    t = time.perf_counter() - t0
+    out = {"workload": "tiny fp32 decoder, block Jacobi n=8, 64 new tokens", "iterations": len(acc),
+           "tpf": round(len(toks) / len(acc), 3), "us_per_iteration_wall": round(t / len(acc) * 1e6, 1)}
+    log(f"tiny: {out}")
+    return out
+
+
+def bench_n32(model, dec, shape, prompt_len=1024, steps=10, warmup=3):
+    import torch
+    from paper_2512_14681_amd import decode
+    import jf_inputs
+    n, V = 32, shape["vocab"]
+    dec.reset()
+    p = dec.prefill(jf_inputs.prompt(1, prompt_len, V))
+    d_draft = torch.tensor([p] + [decode.pad_token(2, prompt_len + i, V) for i in range(1, n)],
+                           dtype=torch.int32, device="cuda")
+    d_arg = torch.zeros(n, dtype=torch.int32, device="cuda")
+    d_res = torch.zeros((warmup + steps, 4), dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+
+    def step(i):
+        model.jf_jacobi_step(d_draft, n, 1, 2, d_arg, d_res[i], d_draft)
+        model.jf_commit_kv(None, d_res[i])
+    for i in range(warmup):
+        step(i)
+    us = _time_calls(lambda i: step(warmup + i), steps, st)
+    acc = d_res[warmup:, 0].cpu().numpy()
+    sb = step_bytes(shape, n, prompt_len + int(acc.sum()) // 2)
+    out = {"workload": "7B-shaped decoder, Jacobi step n=32 running window, 1024-token prefix",
+           "step_us": round(us, 1), "tpf": round(float(acc.mean()), 4),
+           "tokens_s": round(float(acc.mean()) / us * 1e6, 2),
+           "step_hbm_frac": round(sb / us / 1e3 / HBM_PEAK_GBS, 4)}
+    log(f"n=32: {out}")
+    return out
+
+
+def bench_multiblock(model, dec, shape, prefix=2048, new_tokens=64, reps=10):
+    """Multi-block decoding with rejection recycling (K = 4 blocks of n = 16,
+    r = 0.85, up to 8 recycled 16-token candidates) after a 2048-token
+    prompt; and the largest step of that configuration, R = 192 rows (the
+    real-active draft, 3 pseudo-active blocks, 8 candidates) under the tree
+    mask, timed without committing."""
+    import numpy as np
+    import torch
+    import jf_inputs
+    from paper_2512_14681_amd import decode, jf
+    V = shape["vocab"]
+    prompt = jf_inputs.prompt(3, prefix, V)
+    dec.reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    dec.prefill(prompt)
+    t_prefill = time.perf_counter() - t0
+    dec.reset()
+    t0 = time.perf_counter()
+    toks, trace = dec.generate_multiblock(prompt, 16, 4, 0.85, new_tokens, n_cand=8, cand_len=16)
+    t = time.perf_counter() - t0 - t_prefill
+    Rs = [tr["R"] for tr in trace]
+    natural = {"new_tokens": len(toks), "iterations": len(trace), "tpf": round(len(toks) / len(trace), 3),
+               "rows_per_step_mean": round(float(np.mean(Rs)), 1), "rows_per_step_max": int(max(Rs)),
+               "ms_per_iteration_wall": round(t / len(trace) * 1e3, 3),
+               "note": "wall clock per iteration (prefill subtracted), incl. the host-side policy "
+                       "and the per-iteration result read"}
+    # the largest step shape, timed on the device
+    dec.reset()
+    p = dec.prefill(prompt)
+    n, R = 16, 192
+    segs = [(0, n, -1, jf.JF_ROLE_RA, 1)]
+    for b in range(1, 4):
+        segs.append((b * n, n, b * n - 1, jf.JF_ROLE_PSEUDO, 0))
+    for c in range(8):
+        segs.append((64 + c * n, n, 0, jf.JF_ROLE_CAND, 0))
+    rng = np.random.default_rng(5)
+    tokens = [p] + [int(t) for t in rng.integers(0, V, R - 1)]
+    d_tok = torch.tensor(tokens, dtype=torch.int32, device="cuda")
+    d_arg = torch.zeros(R, dtype=torch.int32, device="cuda")
+    d_seg = torch.zeros(jf.JF_MAX_SEGMENTS, dtype=torch.int32, device="cuda")
+    d_res = torch.zeros(4, dtype=torch.int32, device="cuda")
+    d_path = torch.zeros(R, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+    call = lambda i: model.jf_multiblock_step(d_tok, R, segs, d_arg, d_seg, d_res, d_path)
+    for i in range(3):
+        call(i)
+    us = _time_calls(call, reps, st)
+    d, F, H, G, hd, Lr = (shape[k] for k in ("d_model", "d_ffn", "n_heads", "n_kv_heads", "head_dim", "n_layers"))
+    params = Lr * ((H + 2 * G) * hd * d + d * H * hd + 3 * F * d) + V * d
+    flops = 2 * params * R + Lr * 4 * R * (prefix + R) * hd * H
+    sb = step_bytes(shape, R, prefix)
+    step = {"rows": R, "step_us": round(us, 1), "mfma_frac_bf16": round(flops / us / 1e6 / 2.5e3, 4),
+            "step_hbm_frac": round(sb / us / 1e3 / HBM_PEAK_GBS, 4), "tflop_s": round(flops / us / 1e6, 1)}
+    out = {"workload": "7B-shaped decoder, multi-block K=4 x n=16 + up to 8 recycled candidates, "
+                       "2048-token prefix", "decode": natural, "largest_step": step}
+    log(f"multi-block: {out}")
+    return out
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -133,6 +354,8 @@ def main():
                     help="skip the per-kernel event pass (for hardware-counter runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 256 MiB device-to-device 3 times (counter calibration)")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="skip the other workloads (configs 1, 2, 3, 4 at n=32, 5)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the Jacobi step runs on a single MI355X and this "
@@ -161,7 +384,7 @@ def main():
     t0 = time.time()
     w = jf_inputs.model_weights(shape, seed=0)
     log(f"weights generated in {time.time() - t0:.1f}s")
-    max_ctx = ((args.prompt + n * (W + 2 * K + 4) + 63) // 64) * 64
+    max_ctx = ((max(args.prompt + n * (W + 2 * K + 4), 2048 + 64 + 256 + 256) + 63) // 64) * 64
     model = jf.Model(shape, w, max_rows=256, max_ctx=max_ctx)
     del w
     log(f"model loaded ({time.time() - t0:.1f}s)")
@@ -246,6 +469,16 @@ def main():
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
         "roofline": roofline,
     }
+    if not args.headline_only:
+        others = {}
+        others["config4_n32"] = bench_n32(model, dec, shape)
+        others["config5_multiblock"] = bench_multiblock(model, dec, shape)
+        del model, dec
+        torch.cuda.empty_cache()
+        others["config2_attention"] = bench_attention()
+        others["config3_lm_head_accept"] = bench_lm_head()
+        others["config1_tiny"] = bench_tiny()
+        out["other_workloads"] = others
     if not args.no_cpu_baseline:
         t2 = time.time()
         out["cpu_baseline"] = cpu_baseline(shape, n, args.prompt, tpf)

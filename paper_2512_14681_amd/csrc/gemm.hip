@@ -399,11 +399,29 @@ static void plan_few_rows(GemmShape& s, int epi_kind) {
   }
 }
 
+// Residual projections (O and down) with <= 16 rows: 64-column groups of 8
+// waves split K across 4 blocks when K allows 7+ K-blocks per block (step
+// latency measured on the 7B shapes: the O projection gains ~0.6 us per call
+// over the narrow-group plan; fewer blocks run the residual / next-norm
+// epilogue).
+static bool plan_residual(GemmShape& s) {
+  const int KC = s.K / 128;
+  if (s.R > 16 || s.N % 64 || KC < 28) return false;
+  const int groups = s.N / 64;
+  if (groups > (int)kGemmCounters || (size_t)groups * 4 * s.R * 64 > kGemmPartFloats) return false;
+  s.NT = 4;
+  s.WK = 8;
+  s.S = 4;
+  s.D = 0;
+  return true;
+}
+
 void gemm_plan(GemmShape& s, int epi_kind) {
   const int KC = s.K / 128;
   const int RT = round_rt(s.R);
   s.D = 0;
   s.NT = 0;
+  if (epi_kind == EPI_RESID && plan_residual(s)) return;
   if (RT <= 2) {
     plan_few_rows(s, epi_kind);
     if (s.NT > 0) return;
