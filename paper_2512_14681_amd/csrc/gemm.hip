@@ -16,36 +16,36 @@
 
 namespace jf {
 
-// Runs on the reduced output tile of column group ng (NT * 16 columns),
-// tile[row * tld + c], with threads tid = 0..nth-1 sharing the work.
+// Runs on output rows r0 .. r0 + R - 1 of column group ng (NT * 16
+// columns), held in tile[(row - r0) * tld + c], with threads tid = 0..nth-1
+// sharing the work.
 template <typename T>
 __device__ __forceinline__ void epilogue(float* tile, int tld, int NT, const Epi& ep, int ng,
-                                         int tid, int nth) {
+                                         int tid, int nth, int r0, int R) {
   const int cols = NT * 16;
-  const int R = ep.R;
   if (ep.kind == EPI_RESID && ep.gain_next) {
     // Residual add, then the next RMSNorm's input: (new h) * gain as
     // activation planes, and the row's sum of squares over these columns.
     T* xg = reinterpret_cast<T*>(ep.xg);
     for (int e = tid; e < R * cols; e += nth) {
-      const int row = e / cols, c = e - row * cols;
+      const int row = r0 + e / cols, c = e % cols;
       const int col = ng * cols + c;
       float* dst = ep.f32 + (size_t)row * ep.ldf + col;
-      const float hn = *dst + tile[row * tld + c];
+      const float hn = *dst + tile[(row - r0) * tld + c];
       *dst = hn;
       act_store<T>(xg + act_offset(row, col, ep.ldf), ep.xg_plane, hn * ep.gain_next[col]);
-      tile[row * tld + c] = hn * hn;
+      tile[(row - r0) * tld + c] = hn * hn;
     }
     __syncthreads();
-    for (int row = tid; row < R; row += nth) {
+    for (int row = r0 + tid; row < r0 + R; row += nth) {
       float p = 0.f;
-      for (int c = 0; c < cols; ++c) p += tile[row * tld + c];
+      for (int c = 0; c < cols; ++c) p += tile[(row - r0) * tld + c];
       ss_add(ep.ss_out, ep.ss_stride, row, p);
     }
   } else if (ep.kind == EPI_STORE || ep.kind == EPI_RESID) {
     for (int e = tid; e < R * cols; e += nth) {
-      int row = e / cols, c = e - row * cols;
-      float v = tile[row * tld + c];
+      int row = r0 + e / cols, c = e % cols;
+      float v = tile[(row - r0) * tld + c];
       float* dst = ep.f32 + (size_t)row * ep.ldf + (size_t)ng * cols + c;
       if (ep.kind == EPI_RESID) *dst += v; else *dst = v;
     }
@@ -53,26 +53,26 @@ __device__ __forceinline__ void epilogue(float* tile, int tld, int NT, const Epi
     const int half_cols = cols / 2;  // features per block
     T* act = reinterpret_cast<T*>(ep.act);
     for (int e = tid; e < R * half_cols; e += nth) {
-      int row = e / half_cols, f = e - row * half_cols;
+      int row = r0 + e / half_cols, f = e % half_cols;
       int p = f >> 4, c = f & 15;
-      float gt = tile[row * tld + (2 * p) * 16 + c];
-      float up = tile[row * tld + (2 * p + 1) * 16 + c];
+      float gt = tile[(row - r0) * tld + (2 * p) * 16 + c];
+      float up = tile[(row - r0) * tld + (2 * p + 1) * 16 + c];
       float s = gt / (1.0f + __expf(-gt));
       act_store<T>(act + act_offset(row, ng * half_cols + f, ep.act_k), ep.act_plane, s * up);
     }
   } else if (ep.kind == EPI_ARGMAX) {
-    for (int row = tid; row < R; row += nth) {
+    for (int row = r0 + tid; row < r0 + R; row += nth) {
       uint64_t best = 0;
       for (int c = 0; c < cols; ++c) {
-        uint64_t k = argmax_key(tile[row * tld + c], (uint32_t)(ng * cols + c));
+        uint64_t k = argmax_key(tile[(row - r0) * tld + c], (uint32_t)(ng * cols + c));
         best = k > best ? k : best;
       }
       ep.part[(size_t)ng * ep.part_stride + row] = best;
     }
     if (ep.logits) {
       for (int e = tid; e < R * cols; e += nth) {
-        int row = e / cols, c = e - row * cols;
-        ep.logits[(size_t)row * ep.ldl + (size_t)ng * cols + c] = tile[row * tld + c];
+        int row = r0 + e / cols, c = e % cols;
+        ep.logits[(size_t)row * ep.ldl + (size_t)ng * cols + c] = tile[(row - r0) * tld + c];
       }
     }
   } else if (ep.kind == EPI_QKV) {
@@ -82,17 +82,17 @@ __device__ __forceinline__ void epilogue(float* tile, int tld, int NT, const Epi
     T* kv = reinterpret_cast<T*>(ep.kv);
     const size_t page_elems = (size_t)2 * G * kPage * hd;
     for (int e = tid; e < R * cols; e += nth) {
-      int row = e / cols, c = e - row * cols;
+      int row = r0 + e / cols, c = e % cols;
       int pr = ng * cols + c;         // packed row
       int head = pr / hd, w = pr - head * hd;
-      float x = tile[row * tld + c];
+      float x = tile[(row - r0) * tld + c];
       float out;
       int dim;
       if (head < H + G) {
         int t = w >> 4, cc = w & 15;
         int i = 8 * t + (cc & 7);
         dim = cc < 8 ? i : half + i;
-        float y = tile[row * tld + (c ^ 8)];
+        float y = tile[(row - r0) * tld + (c ^ 8)];
         int pos = ep.pos[row];
         float cs = ep.rope_cos[(size_t)pos * half + i];
         float sn = ep.rope_sin[(size_t)pos * half + i];
@@ -140,17 +140,38 @@ template <typename T, int RT, int NT, int WK> struct Ring {
   static constexpr int D = kD < 1 ? 1 : (kD > 4 ? 4 : kD);
 };
 
-template <typename T, int RT, int NT, int WK, int D = Ring<T, RT, NT, WK>::D>
+// Grid: one block per (column group, K split, row chunk).  More than 32 rows
+// are done in chunks of 32 (C of them), each by its own block with the
+// weights of its unit (column group, K split) streamed again; the block
+// order is XCD-aware so that those re-reads hit L2: linear block b runs on
+// XCD b % 8 (round-robin dispatch), so the C chunks of a unit get ids
+// congruent mod 8 and adjacent in dispatch order, i.e. the same XCD at the
+// same time, and the unit's weights come from HBM once.
+// CHUNKED (C > 1): the 1-D XCD-aware block order above, and the weights,
+// read by the C chunk blocks of a unit, are loaded with the ordinary
+// (L2-allocating) policy instead of the streaming hint.  Otherwise the grid
+// is (column groups, K splits) and there is one chunk.
+template <typename T, int RT, int NT, int WK, int D = Ring<T, RT, NT, WK>::D, bool CHUNKED = false>
 __global__ void __launch_bounds__(64 * WK)
-k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC, int P, Epi ep) {
+k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC, int P, int groups,
+       int S, int C, Epi ep) {
   extern __shared__ float lds[];
   constexpr bool PX = Ring<T, RT, NT, WK>::kPrefetchX;
   constexpr int RX = PX ? RT : 1;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int ng = blockIdx.x;
-  const int ks = blockIdx.y, S = gridDim.y;
-  const int R = ep.R;
+  int z = 0, ng = blockIdx.x, ks = blockIdx.y;
+  if constexpr (CHUNKED) {
+    const int b = blockIdx.x;
+    z = (b >> 3) % C;                              // row chunk
+    const int u = ((b >> 3) / C) * 8 + (b & 7);    // unit: column group + K split
+    if (u >= groups * S) return;                   // ids past the last unit (block-uniform)
+    ng = u % groups;
+    ks = u / groups;
+  }
+  const int rb = 32 * z;                           // the chunk's first output row
+  const int Rs = CHUNKED ? 32 : ep.R;              // rows per chunk (partial-tile stride)
+  const int R = CHUNKED ? min(32, ep.R - rb) : ep.R;  // rows of this chunk
   const int kb0 = (KC * ks) / S, kb1 = (KC * (ks + 1)) / S;   // this block's K-blocks
   const int kc0 = kb0 + ((kb1 - kb0) * wave) / WK;
   const int kc1 = kb0 + ((kb1 - kb0) * (wave + 1)) / WK;
@@ -161,8 +182,8 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
   // behind the weight stream.
   const bool ss_early = ep.ss_in && R <= (int)blockDim.x;
   uint64_t ssw[3] = {0, 0, 0};
-  if (ss_early && (int)threadIdx.x < R) ss_load(ep.ss_in, ep.ss_stride, ep.row0 + threadIdx.x, ssw);
-  if (ep.ss_clear && blockIdx.x == 0 && blockIdx.y == 0)
+  if (ss_early && (int)threadIdx.x < R) ss_load(ep.ss_in, ep.ss_stride, ep.row0 + rb + threadIdx.x, ssw);
+  if (ep.ss_clear && ng == 0 && ks == 0 && z == 0)
     for (int i = threadIdx.x; i < 3 * ep.ss_stride; i += blockDim.x)
       __hip_atomic_store(ep.ss_clear + i, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
@@ -187,7 +208,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
   // Rows past R read row R-1 instead (no per-lane branch): MFMA rows are
   // independent and padding rows are never stored.
   auto xload = [&](int kc, int mt, ActFrag<T> (&x)[4]) {
-    const int row = ep.row0 + min(mt * 16 + lrow, R - 1);
+    const int row = ep.row0 + rb + min(mt * 16 + lrow, R - 1);
     const T* xp = X + act_offset(row, kc * 128 + koff, KC * 128);
 #pragma unroll
     for (int j = 0; j < 4; ++j) x[j] = act_load<T>(xp + j * 512, xplane);
@@ -202,7 +223,8 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        w[nt][j] = frag_load_nt<T>(wb + toff[nt] + kc * kstride + j * 512);
+        w[nt][j] = CHUNKED ? frag_load<T>(wb + toff[nt] + kc * kstride + j * 512)
+                          : frag_load_nt<T>(wb + toff[nt] + kc * kstride + j * 512);
     if constexpr (PX) {
 #pragma unroll
       for (int mt = 0; mt < RT; ++mt) xload(kc, mt, x[mt]);
@@ -290,7 +312,8 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     // increment, and the last block reads them after seeing the count.
     __shared__ int s_last;
     const int cols = NT * 16;
-    float* mine = ep.kpart + ((size_t)ng * S + ks) * (size_t)(R * cols);
+    const size_t unit_part = ((size_t)ng * C + z) * S;  // this chunk's S partial tiles
+    float* mine = ep.kpart + (unit_part + ks) * (size_t)(Rs * cols);
     for (int e = threadIdx.x; e < R * cols; e += 64 * WK) {
       const int row = e / cols, c = e - row * cols;
       __hip_atomic_store(mine + e, tile[row * tld + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -298,13 +321,13 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's stores are done
     __syncthreads();
     if (threadIdx.x == 0)
-      s_last = __hip_atomic_fetch_add(ep.kcount + ng, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+      s_last = __hip_atomic_fetch_add(ep.kcount + ng * C + z, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
     __syncthreads();
     if (!s_last) return;
     // Loads are issued four splits at a time so that their latencies
     // overlap; the sum keeps split order.
-    const float* all = ep.kpart + (size_t)ng * S * (size_t)(R * cols);
-    const size_t pstride = (size_t)R * cols;
+    const float* all = ep.kpart + unit_part * (size_t)(Rs * cols);
+    const size_t pstride = (size_t)Rs * cols;
     for (int e = threadIdx.x; e < R * cols; e += 64 * WK) {
       float sum = 0.f;
       int k = 0;
@@ -321,11 +344,11 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
       const int row = e / cols, c = e - row * cols;
       tile[row * tld + c] = sum;
     }
-    if (threadIdx.x == 0) __hip_atomic_store(ep.kcount + ng, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) __hip_atomic_store(ep.kcount + ng * C + z, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
   }
   if (ep.ss_in) {
-    // Output row r times 1 / rms(h[row0 + r]): the normalisation commutes
+    // Output row r times 1 / rms(h[row0 + rb + r]): the normalisation commutes
     // with the contraction (a per-row scale of X).
     __shared__ float s_rs[256];
     if (ss_early) {
@@ -333,7 +356,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     } else {
       for (int row = threadIdx.x; row < R; row += blockDim.x) {
         uint64_t w[3];
-        ss_load(ep.ss_in, ep.ss_stride, ep.row0 + row, w);
+        ss_load(ep.ss_in, ep.ss_stride, ep.row0 + rb + row, w);
         s_rs[row] = ss_rstd(w, ep.norm_inv_d, ep.norm_eps);
       }
     }
@@ -345,7 +368,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     }
     __syncthreads();
   }
-  epilogue<T>(tile, tld, NT, ep, ng, threadIdx.x, blockDim.x);
+  epilogue<T>(tile, tld, NT, ep, ng, threadIdx.x, blockDim.x, rb, R);
 }
 
 static int round_rt(int R) {
@@ -417,34 +440,41 @@ static bool plan_residual(GemmShape& s) {
 }
 
 void gemm_plan(GemmShape& s, int epi_kind) {
-  const int KC = s.K / 128;
-  const int RT = round_rt(s.R);
+  // More than 32 rows run as 32-row chunks (see k_gemm), each planned as 32 rows.
+  const int R = s.R;
+  s.R = std::min(R, 32);
   s.D = 0;
   s.NT = 0;
-  if (epi_kind == EPI_RESID && plan_residual(s)) return;
-  if (RT <= 2) {
-    plan_few_rows(s, epi_kind);
-    if (s.NT > 0) return;
-  }
-  // More rows: the activation tiles dominate registers and LDS; no split-K.
-  s.NT = epi_kind == EPI_SWIGLU ? 2 : 1;
-  const int groups = s.N / (16 * s.NT);
-  int wk = 1;
-  while (wk < 8 && groups * wk < 2048 && KC / (wk * 2) >= 2) wk *= 2;
-  while (wk > 1 && lds_bytes(RT, s.NT, wk) > 65536) wk /= 2;
-  s.WK = wk;
-  s.S = 1;
+  if (!(epi_kind == EPI_RESID && plan_residual(s))) plan_few_rows(s, epi_kind);
+  s.R = R;
+  s.C = R > 32 ? (R + 31) / 32 : 1;
+  // split-K scratch for all chunks (32-row partial tiles when chunked)
+  const size_t rows = s.C > 1 ? (size_t)32 * s.C : (size_t)R;
+  if (s.S > 1 && ((size_t)s.N * s.S * rows > kGemmPartFloats ||
+                  (size_t)(s.N / (16 * s.NT)) * s.C > kGemmCounters))
+    s.S = 1;
 }
 
 size_t gemm_blocks(const GemmShape& s) { return (size_t)s.N / (16 * s.NT); }
+
+static unsigned grid_blocks(const GemmShape& s) {
+  const int units = s.N / (16 * s.NT) * s.S;
+  return (unsigned)((units + 7) / 8 * 8 * s.C);
+}
 
 template <typename T, int RT, int NT, int WK, int D>
 static hipError_t launch_t(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
                            const Epi& ep, hipStream_t st) {
   size_t lds = lds_bytes(RT, NT, WK);
-  dim3 grid((unsigned)(s.N / (16 * NT)), (unsigned)s.S), block(64 * WK);
-  hipLaunchKernelGGL((k_gemm<T, RT, NT, WK, D>), grid, block, lds, st, reinterpret_cast<const T*>(X),
-                     xplane, reinterpret_cast<const T*>(Wp), s.K / 128, pack_group(s.N), ep);
+  const int groups = s.N / (16 * NT);
+  if (s.C > 1)
+    hipLaunchKernelGGL((k_gemm<T, RT, NT, WK, D, true>), dim3(grid_blocks(s)), dim3(64 * WK), lds, st,
+                       reinterpret_cast<const T*>(X), xplane, reinterpret_cast<const T*>(Wp), s.K / 128,
+                       pack_group(s.N), groups, s.S, s.C, ep);
+  else
+    hipLaunchKernelGGL((k_gemm<T, RT, NT, WK, D, false>), dim3(groups, s.S), dim3(64 * WK), lds, st,
+                       reinterpret_cast<const T*>(X), xplane, reinterpret_cast<const T*>(Wp), s.K / 128,
+                       pack_group(s.N), groups, s.S, 1, ep);
   return hipGetLastError();
 }
 
@@ -483,26 +513,23 @@ static hipError_t launch_nt(const void* X, size_t xplane, const void* Wp, const 
 template <typename T>
 static hipError_t launch_rt(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
                             const Epi& ep, hipStream_t st) {
-  switch (round_rt(s.R)) {
-    case 1: return launch_nt<T, 1>(X, xplane, Wp, s, ep, st);
-    case 2: return launch_nt<T, 2>(X, xplane, Wp, s, ep, st);
-    case 4: return launch_nt<T, 4>(X, xplane, Wp, s, ep, st);
-    case 8: return launch_nt<T, 8>(X, xplane, Wp, s, ep, st);
-    case 12: return launch_nt<T, 12>(X, xplane, Wp, s, ep, st);
-    case 16: return launch_nt<T, 16>(X, xplane, Wp, s, ep, st);
-    default: return hipErrorInvalidValue;
-  }
+  // row tiles per block: 1 or 2 (more rows are chunked)
+  if (s.C > 1 || s.R > 16) return launch_nt<T, 2>(X, xplane, Wp, s, ep, st);
+  return launch_nt<T, 1>(X, xplane, Wp, s, ep, st);
 }
 
 hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
                        const GemmShape& s, const Epi& ep, hipStream_t st) {
   if (s.R < 1 || s.R > 256 || s.K < 128 || s.K % 128 || s.N < 16 * s.NT || s.N % (16 * s.NT))
     return hipErrorInvalidValue;
+  if (s.C != (s.R > 32 ? (s.R + 31) / 32 : 1)) return hipErrorInvalidValue;
   if (s.S < 1 || s.S > s.K / 128) return hipErrorInvalidValue;
-  if (s.S > 1 && (!ep.kpart || !ep.kcount || s.N / (16 * s.NT) > (int)kGemmCounters ||
-                  (size_t)(s.N / 16) * s.S * s.R * 16 > kGemmPartFloats))
+  const size_t rows = s.C > 1 ? (size_t)32 * s.C : (size_t)s.R;
+  if (s.S > 1 && (!ep.kpart || !ep.kcount || (size_t)(s.N / (16 * s.NT)) * s.C > kGemmCounters ||
+                  (size_t)s.N * s.S * rows > kGemmPartFloats))
     return hipErrorInvalidValue;
-  if (lds_bytes(round_rt(s.R), s.NT, s.WK) > 65536) return hipErrorInvalidValue;
+  if (s.C > 1 && ep.row0 != 0) return hipErrorInvalidValue;
+  if (lds_bytes(s.C > 1 ? 2 : round_rt(s.R), s.NT, s.WK) > 65536) return hipErrorInvalidValue;
   return dtype == 1 ? launch_rt<bf16_t>(X, xplane, Wp, s, ep, st)
                     : launch_rt<float>(X, xplane, Wp, s, ep, st);
 }

@@ -78,13 +78,15 @@ struct GemmShape {
   int NT, WK;    // 16-column tiles per block, waves splitting K per block
   int S;         // blocks splitting K per column group
   int D;         // register-ring depth (0: the kernel's default)
+  int C;         // row chunks of at most 32 rows (blocks per column group and split)
 };
 
 // Scratch a GEMM needs for split-K partials (floats) and counters (ints).
 constexpr size_t kGemmPartFloats = (size_t)16 << 20;  // 64 MB
 constexpr size_t kGemmCounters = 16384;
 
-// Chooses NT / WK / S for a shape (NT fixed by the epilogue where it matters).
+// Chooses NT / WK / S / C for a shape (NT fixed by the epilogue where it
+// matters).
 void gemm_plan(GemmShape& s, int epi_kind);
 // X: activation planes of an [R][K] matrix in the GEMM-input layout
 // (act_offset; planes xplane elements apart for bf16 models).
