@@ -72,7 +72,7 @@ __device__ __forceinline__ uint32_t low_bits8(int n) {
 }
 
 template <typename T, int HD>
-__global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
+__global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
   constexpr int NW = 4;  // waves per block
   __shared__ float s_m[NW][16], s_l[NW][16];
   __shared__ float s_o[NW][16][HD + 4];

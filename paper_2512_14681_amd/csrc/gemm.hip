@@ -169,9 +169,10 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     ng = u % groups;
     ks = u / groups;
   }
-  const int rb = 32 * z;                           // the chunk's first output row
-  const int Rs = CHUNKED ? 32 : ep.R;              // rows per chunk (partial-tile stride)
-  const int R = CHUNKED ? min(32, ep.R - rb) : ep.R;  // rows of this chunk
+  constexpr int CR = 16 * RT;                      // rows per chunk when chunked
+  const int rb = CR * z;                           // the chunk's first output row
+  const int Rs = CHUNKED ? CR : ep.R;              // rows per chunk (partial-tile stride)
+  const int R = CHUNKED ? min(CR, ep.R - rb) : ep.R;  // rows of this chunk
   const int kb0 = (KC * ks) / S, kb1 = (KC * (ks + 1)) / S;   // this block's K-blocks
   const int kc0 = kb0 + ((kb1 - kb0) * wave) / WK;
   const int kc1 = kb0 + ((kb1 - kb0) * (wave + 1)) / WK;
@@ -371,6 +372,11 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
   epilogue<T>(tile, tld, NT, ep, ng, threadIdx.x, blockDim.x, rb, R);
 }
 
+// Rows per chunk of a GEMM with more rows than that: 32 (2 row tiles per
+// wave).  16-row chunks were measured slower on the 7B step (+0.6 ms at 32
+// rows, +1.2 ms at 192).
+constexpr int kChunkRows = 32;
+
 static int round_rt(int R) {
   int rt = (R + 15) / 16;
   if (rt <= 2) return rt;
@@ -440,16 +446,17 @@ static bool plan_residual(GemmShape& s) {
 }
 
 void gemm_plan(GemmShape& s, int epi_kind) {
-  // More than 32 rows run as 32-row chunks (see k_gemm), each planned as 32 rows.
+  // More than kChunkRows rows run as chunks of kChunkRows (see k_gemm), each
+  // planned as a kChunkRows-row GEMM.
   const int R = s.R;
-  s.R = std::min(R, 32);
+  s.R = std::min(R, kChunkRows);
   s.D = 0;
   s.NT = 0;
   if (!(epi_kind == EPI_RESID && plan_residual(s))) plan_few_rows(s, epi_kind);
   s.R = R;
-  s.C = R > 32 ? (R + 31) / 32 : 1;
-  // split-K scratch for all chunks (32-row partial tiles when chunked)
-  const size_t rows = s.C > 1 ? (size_t)32 * s.C : (size_t)R;
+  s.C = R > kChunkRows ? (R + kChunkRows - 1) / kChunkRows : 1;
+  // split-K scratch for all chunks (kChunkRows-row partial tiles when chunked)
+  const size_t rows = s.C > 1 ? (size_t)kChunkRows * s.C : (size_t)R;
   if (s.S > 1 && ((size_t)s.N * s.S * rows > kGemmPartFloats ||
                   (size_t)(s.N / (16 * s.NT)) * s.C > kGemmCounters))
     s.S = 1;
@@ -514,7 +521,8 @@ template <typename T>
 static hipError_t launch_rt(const void* X, size_t xplane, const void* Wp, const GemmShape& s,
                             const Epi& ep, hipStream_t st) {
   // row tiles per block: 1 or 2 (more rows are chunked)
-  if (s.C > 1 || s.R > 16) return launch_nt<T, 2>(X, xplane, Wp, s, ep, st);
+  const int rt = s.C > 1 ? kChunkRows / 16 : (s.R > 16 ? 2 : 1);
+  if (rt == 2) return launch_nt<T, 2>(X, xplane, Wp, s, ep, st);
   return launch_nt<T, 1>(X, xplane, Wp, s, ep, st);
 }
 
@@ -522,14 +530,14 @@ hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
                        const GemmShape& s, const Epi& ep, hipStream_t st) {
   if (s.R < 1 || s.R > 256 || s.K < 128 || s.K % 128 || s.N < 16 * s.NT || s.N % (16 * s.NT))
     return hipErrorInvalidValue;
-  if (s.C != (s.R > 32 ? (s.R + 31) / 32 : 1)) return hipErrorInvalidValue;
+  if (s.C != (s.R > kChunkRows ? (s.R + kChunkRows - 1) / kChunkRows : 1)) return hipErrorInvalidValue;
   if (s.S < 1 || s.S > s.K / 128) return hipErrorInvalidValue;
-  const size_t rows = s.C > 1 ? (size_t)32 * s.C : (size_t)s.R;
+  const size_t rows = s.C > 1 ? (size_t)kChunkRows * s.C : (size_t)s.R;
   if (s.S > 1 && (!ep.kpart || !ep.kcount || (size_t)(s.N / (16 * s.NT)) * s.C > kGemmCounters ||
                   (size_t)s.N * s.S * rows > kGemmPartFloats))
     return hipErrorInvalidValue;
   if (s.C > 1 && ep.row0 != 0) return hipErrorInvalidValue;
-  if (lds_bytes(s.C > 1 ? 2 : round_rt(s.R), s.NT, s.WK) > 65536) return hipErrorInvalidValue;
+  if (lds_bytes(s.C > 1 ? kChunkRows / 16 : round_rt(s.R), s.NT, s.WK) > 65536) return hipErrorInvalidValue;
   return dtype == 1 ? launch_rt<bf16_t>(X, xplane, Wp, s, ep, st)
                     : launch_rt<float>(X, xplane, Wp, s, ep, st);
 }
