@@ -445,6 +445,17 @@ static bool plan_residual(GemmShape& s) {
   return true;
 }
 
+// Plans measured at the step level for the 7B-shaped projections with 17-32
+// rows (2 row tiles per wave).  The rule above over-splits the long-K down
+// projection and under-populates the wide ones at this row count.
+struct MeasuredPlan { int epi, N, K, NT, WK, S; };
+static const MeasuredPlan kPlans32[] = {
+    {EPI_RESID, 3584, 18944, 4, 4, 4},    // down: -107 us per n = 32 step vs the rule
+    {EPI_RESID, 3584, 3584, 2, 8, 2},     // O: -29 us
+    {EPI_SWIGLU, 37888, 3584, 4, 4, 1},   // gate/up: -32 us
+    {EPI_ARGMAX, 152064, 3584, 4, 4, 1},  // LM head: -16 us
+};
+
 void gemm_plan(GemmShape& s, int epi_kind) {
   // More than kChunkRows rows run as chunks of kChunkRows (see k_gemm), each
   // planned as a kChunkRows-row GEMM.
@@ -452,7 +463,14 @@ void gemm_plan(GemmShape& s, int epi_kind) {
   s.R = std::min(R, kChunkRows);
   s.D = 0;
   s.NT = 0;
-  if (!(epi_kind == EPI_RESID && plan_residual(s))) plan_few_rows(s, epi_kind);
+  bool measured = false;
+  if (R > 16 && R <= 32)  // unchunked only: as chunk plans they measured no better
+    for (const MeasuredPlan& m : kPlans32)
+      if (m.epi == epi_kind && m.N == s.N && m.K == s.K) {
+        s.NT = m.NT; s.WK = m.WK; s.S = m.S; s.D = 0;
+        measured = true;
+      }
+  if (!measured && !(epi_kind == EPI_RESID && plan_residual(s))) plan_few_rows(s, epi_kind);
   s.R = R;
   s.C = R > kChunkRows ? (R + kChunkRows - 1) / kChunkRows : 1;
   // split-K scratch for all chunks (kChunkRows-row partial tiles when chunked)
