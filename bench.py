@@ -254,11 +254,11 @@ def bench_tiny():
     return out
 
 
-def bench_n32(model, dec, shape, prompt_len=1024, steps=10, warmup=3):
+def bench_window(model, dec, shape, n, prompt_len=1024, steps=10, warmup=3):
     import torch
     from paper_2512_14681_amd import decode
     import jf_inputs
-    n, V = 32, shape["vocab"]
+    V = shape["vocab"]
     dec.reset()
     p = dec.prefill(jf_inputs.prompt(1, prompt_len, V))
     d_draft = torch.tensor([p] + [decode.pad_token(2, prompt_len + i, V) for i in range(1, n)],
@@ -275,11 +275,11 @@ def bench_n32(model, dec, shape, prompt_len=1024, steps=10, warmup=3):
     us = _time_calls(lambda i: step(warmup + i), steps, st)
     acc = d_res[warmup:, 0].cpu().numpy()
     sb = step_bytes(shape, n, prompt_len + int(acc.sum()) // 2)
-    out = {"workload": "7B-shaped decoder, Jacobi step n=32 running window, 1024-token prefix",
+    out = {"workload": f"7B-shaped decoder, Jacobi step n={n} running window, 1024-token prefix",
            "step_us": round(us, 1), "tpf": round(float(acc.mean()), 4),
            "tokens_s": round(float(acc.mean()) / us * 1e6, 2),
            "step_hbm_frac": round(sb / us / 1e3 / HBM_PEAK_GBS, 4)}
-    log(f"n=32: {out}")
+    log(f"n={n}: {out}")
     return out
 
 
@@ -355,7 +355,7 @@ def main():
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 256 MiB device-to-device 3 times (counter calibration)")
     ap.add_argument("--headline-only", action="store_true",
-                    help="skip the other workloads (configs 1, 2, 3, 4 at n=32, 5)")
+                    help="skip the other workloads (configs 1, 2, 3, 4 at n=32 and 64, 5)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the Jacobi step runs on a single MI355X and this "
@@ -471,7 +471,8 @@ def main():
     }
     if not args.headline_only:
         others = {}
-        others["config4_n32"] = bench_n32(model, dec, shape)
+        others["config4_n32"] = bench_window(model, dec, shape, 32)
+        others["config4_n64"] = bench_window(model, dec, shape, 64)
         others["config5_multiblock"] = bench_multiblock(model, dec, shape)
         del model, dec
         torch.cuda.empty_cache()

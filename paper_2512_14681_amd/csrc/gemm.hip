@@ -445,15 +445,23 @@ static bool plan_residual(GemmShape& s) {
   return true;
 }
 
-// Plans measured at the step level for the 7B-shaped projections with 17-32
-// rows (2 row tiles per wave).  The rule above over-splits the long-K down
-// projection and under-populates the wide ones at this row count.
-struct MeasuredPlan { int epi, N, K, NT, WK, S; };
+// Plans measured at the step level for the 7B-shaped projections: with 17-32
+// rows (2 row tiles per wave, one chunk) and with 33-64 rows (two 32-row
+// chunks).  The rule above over-splits the long-K down projection and, once
+// chunked, keeps too many waves per chunk.
+struct MeasuredPlan { int epi, N, K, NT, WK, S, D; };
 static const MeasuredPlan kPlans32[] = {
-    {EPI_RESID, 3584, 18944, 4, 4, 4},    // down: -107 us per n = 32 step vs the rule
-    {EPI_RESID, 3584, 3584, 2, 8, 2},     // O: -29 us
-    {EPI_SWIGLU, 37888, 3584, 4, 4, 1},   // gate/up: -32 us
-    {EPI_ARGMAX, 152064, 3584, 4, 4, 1},  // LM head: -16 us
+    {EPI_RESID, 3584, 18944, 4, 4, 4, 0},    // down: -107 us per n = 32 step vs the rule
+    {EPI_RESID, 3584, 3584, 2, 8, 2, 0},     // O: -29 us
+    {EPI_SWIGLU, 37888, 3584, 4, 4, 1, 0},   // gate/up: -32 us
+    {EPI_ARGMAX, 152064, 3584, 4, 4, 1, 0},  // LM head: -16 us
+};
+static const MeasuredPlan kPlans64[] = {     // per 32-row chunk, C = 2
+    {EPI_RESID, 3584, 18944, 4, 4, 2, 0},    // down: -272 us per n = 64 step vs the rule
+    {EPI_RESID, 3584, 3584, 2, 8, 1, 0},     // O: -195 us
+    {EPI_QKV, 4608, 3584, 4, 4, 1, 0},       // QKV: -134 us
+    {EPI_SWIGLU, 37888, 3584, 4, 2, 1, 2},   // gate/up: -115 us
+    {EPI_ARGMAX, 152064, 3584, 4, 1, 1, 2},  // LM head: -26 us
 };
 
 void gemm_plan(GemmShape& s, int epi_kind) {
@@ -464,12 +472,17 @@ void gemm_plan(GemmShape& s, int epi_kind) {
   s.D = 0;
   s.NT = 0;
   bool measured = false;
-  if (R > 16 && R <= 32)  // unchunked only: as chunk plans they measured no better
-    for (const MeasuredPlan& m : kPlans32)
-      if (m.epi == epi_kind && m.N == s.N && m.K == s.K) {
-        s.NT = m.NT; s.WK = m.WK; s.S = m.S; s.D = 0;
+  auto lookup = [&](const MeasuredPlan* t, size_t n) {
+    for (size_t i = 0; i < n; ++i)
+      if (t[i].epi == epi_kind && t[i].N == s.N && t[i].K == s.K) {
+        s.NT = t[i].NT; s.WK = t[i].WK; s.S = t[i].S; s.D = t[i].D;
         measured = true;
       }
+  };
+  // each table only where it was measured (the 32-row plans measured no
+  // better as chunk plans)
+  if (R > 16 && R <= 32) lookup(kPlans32, sizeof kPlans32 / sizeof kPlans32[0]);
+  if (R > 32 && R <= 64) lookup(kPlans64, sizeof kPlans64 / sizeof kPlans64[0]);
   if (!measured && !(epi_kind == EPI_RESID && plan_residual(s))) plan_few_rows(s, epi_kind);
   s.R = R;
   s.C = R > kChunkRows ? (R + kChunkRows - 1) / kChunkRows : 1;

@@ -3,7 +3,8 @@
 benchmark times.
 
 * Jacobi step, n = 16 running window after a 1024-token prompt (the benchmark
-  workload): all 16 rows' logits and argmaxes against the oracle.
+  workload), and n = 64 (two 32-row chunks per projection): every row's
+  logits and argmaxes against the oracle.
 * Greedy Jacobi decoding with n = 16 and n = 32: every committed token is the
   oracle's greedy prediction of its position (teacher forcing over the
   committed sequence).
@@ -84,14 +85,16 @@ def prompt1024():
     return jf_inputs.prompt(1, 1024, V)
 
 
-def test_7b_step_n16_window_logits(env, prompt1024):
+@pytest.mark.parametrize("n", [16, 64])
+def test_7b_step_window_logits(env, prompt1024, n):
+    """The benchmark's step (n = 16) and a two-chunk step (n = 64, the
+    projections run as two 32-row chunks): every row's logits and argmax."""
     import torch
     dec, model = env["dec"], env["model"]
     dec.reset()
     p = dec.prefill(prompt1024)
     last = oracle_prefix(env, prompt1024)
     assert p == int(last.argmax()) or gap(last) < GAP_EXEMPT
-    n = 16
     draft = [p] + [ojac.pad_id(2, 1024 + i, V) for i in range(1, n)]
     d_draft = torch.tensor(draft, dtype=torch.int32, device="cuda")
     d_next = torch.zeros(n, dtype=torch.int32, device="cuda")
@@ -101,7 +104,7 @@ def test_7b_step_n16_window_logits(env, prompt1024):
     g = dec.d_argmax[:n].cpu().numpy()
     zo, _ = env["ora"].forward(np.asarray(draft), 1024 + np.arange(n), np.tri(n, dtype=bool))
     err = np.abs(z - zo).max()
-    say(f"n=16 step: max |logit - oracle| = {err:.2e}")
+    say(f"n={n} step: max |logit - oracle| = {err:.2e}")
     assert err < LOGIT_TOL, err
     assert ((g == zo.argmax(1)) | (gap(zo) < GAP_EXEMPT)).all()
     # acceptance against the oracle's own argmax (Eq. 3 / Sec. 3.2)
