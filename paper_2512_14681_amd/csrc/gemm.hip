@@ -446,9 +446,10 @@ static bool plan_residual(GemmShape& s) {
 }
 
 // Plans measured at the step level for the 7B-shaped projections: with 17-32
-// rows (2 row tiles per wave, one chunk) and with 33-64 rows (two 32-row
-// chunks).  The rule above over-splits the long-K down projection and, once
-// chunked, keeps too many waves per chunk.
+// rows (2 row tiles per wave, one chunk), 33-64 rows (two 32-row chunks) and
+// more (three or more chunks).  The rule above over-splits the long-K down
+// projection and, once chunked, keeps too many waves per chunk: the C chunk
+// blocks of a unit already multiply the waves in flight by C.
 struct MeasuredPlan { int epi, N, K, NT, WK, S, D; };
 static const MeasuredPlan kPlans32[] = {
     {EPI_RESID, 3584, 18944, 4, 4, 4, 0},    // down: -107 us per n = 32 step vs the rule
@@ -462,6 +463,13 @@ static const MeasuredPlan kPlans64[] = {     // per 32-row chunk, C = 2
     {EPI_QKV, 4608, 3584, 4, 4, 1, 0},       // QKV: -134 us
     {EPI_SWIGLU, 37888, 3584, 4, 2, 1, 2},   // gate/up: -115 us
     {EPI_ARGMAX, 152064, 3584, 4, 1, 1, 2},  // LM head: -26 us
+};
+static const MeasuredPlan kPlansMany[] = {   // per 32-row chunk, C >= 3 (measured at C = 6, R = 192)
+    {EPI_RESID, 3584, 18944, 4, 4, 2, 0},    // down: -594 us per R = 192 step vs the rule
+    {EPI_RESID, 3584, 3584, 2, 2, 1, 0},     // O: -520 us
+    {EPI_QKV, 4608, 3584, 4, 2, 1, 0},       // QKV: -309 us
+    {EPI_SWIGLU, 37888, 3584, 4, 1, 1, 2},   // gate/up: -569 us
+    {EPI_ARGMAX, 152064, 3584, 4, 1, 1, 2},  // LM head: -77 us
 };
 
 void gemm_plan(GemmShape& s, int epi_kind) {
@@ -483,6 +491,7 @@ void gemm_plan(GemmShape& s, int epi_kind) {
   // better as chunk plans)
   if (R > 16 && R <= 32) lookup(kPlans32, sizeof kPlans32 / sizeof kPlans32[0]);
   if (R > 32 && R <= 64) lookup(kPlans64, sizeof kPlans64 / sizeof kPlans64[0]);
+  if (R > 64) lookup(kPlansMany, sizeof kPlansMany / sizeof kPlansMany[0]);
   if (!measured && !(epi_kind == EPI_RESID && plan_residual(s))) plan_few_rows(s, epi_kind);
   s.R = R;
   s.C = R > kChunkRows ? (R + kChunkRows - 1) / kChunkRows : 1;
