@@ -342,6 +342,64 @@ def bench_multiblock(model, dec, shape, prefix=2048, new_tokens=64, reps=10):
     log(f"multi-block: {out}")
     return out
 
+def bench_trajectory(model, dec, shape, prefix=1024, n=16, blocks=2, sel_blocks=1 << 18, w=16,
+                     copies=4, reps=20):
+    """Trajectory collection (Sec. 2.1) on the 7B-shaped decoder: block-mode
+    decoding of `blocks` blocks of n = 16 after a 1024-token prompt with every
+    iterate recorded on the device; and the noise-schedule point selection
+    (Eq. 7, App. C) over 2^18 synthetic 16-token trajectories (up to 17
+    points each), timed over `copies` rotating device copies so that no
+    launch finds its input in the 256 MB last-level cache."""
+    import numpy as np
+    import torch
+    import jf_inputs
+    from paper_2512_14681_amd import jf
+    V = shape["vocab"]
+    prompt = jf_inputs.prompt(1, prefix, V)
+    dec.reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    dec.prefill(prompt)
+    t_prefill = time.perf_counter() - t0
+    dec.reset()
+    t0 = time.perf_counter()
+    d_traj, lengths = dec.collect_trajectories(prompt, n, blocks)
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0 - t_prefill
+    iters = int((lengths - 1).sum())
+    st = torch.cuda.current_stream()
+    d_a, d_b = torch.zeros(n, dtype=torch.int32, device="cuda"), torch.zeros(n, dtype=torch.int32, device="cuda")
+    rec_us = _time_calls(lambda i: jf.trajectory_record(d_a, d_b, n, n - (i % n), d_a), 200, st)
+    collect = {"blocks": blocks, "n": n, "iterations": iters, "points_recorded": int(lengths.sum()),
+               "ms_per_iteration_wall": round(t / iters * 1e3, 3), "record_kernel_us": round(rec_us, 2),
+               "note": "wall clock per iteration (prefill subtracted): step + record + commit + the "
+                       "per-iteration result read"}
+    # selection
+    t1 = time.time()
+    traj, lens = jf_inputs.trajectories(5, sel_blocks, n, V)
+    log(f"trajectory inputs: {time.time() - t1:.1f}s")
+    P = traj.shape[1]
+    d_src = torch.as_tensor(traj, device="cuda")
+    bufs = [d_src] + [d_src.clone() for _ in range(copies - 1)]
+    d_len = torch.as_tensor(lens, device="cuda")
+    d_sel = torch.zeros(sel_blocks, dtype=torch.int32, device="cuda")
+    call = lambda i: jf.trajectory_select(bufs[i % copies], d_len, sel_blocks, n, P, w, d_sel)
+    for i in range(copies):
+        call(i)
+    us = _time_calls(call, reps, st)
+    nbytes = int(lens.astype(np.int64).sum()) * n * 4 + 8 * sel_blocks
+    gbs = nbytes / us / 1e3
+    select = {"blocks": sel_blocks, "n": n, "w": w, "max_points": P, "mean_points": round(float(lens.mean()), 2),
+              "us": round(us, 2), "bytes_per_launch": nbytes, "GB_s": round(gbs, 1),
+              "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    del bufs, d_src
+    out = {"workload": "trajectory collection: 7B-shaped decoder, block Jacobi n=16 after a 1024-token "
+                       "prefix, every iterate recorded; point selection over 2^18 synthetic 16-token "
+                       "trajectories (Eq. 7, w=16)", "collect": collect, "select": select}
+    log(f"trajectory: {out}")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -474,6 +532,7 @@ def main():
         others["config4_n32"] = bench_window(model, dec, shape, 32)
         others["config4_n64"] = bench_window(model, dec, shape, 64)
         others["config5_multiblock"] = bench_multiblock(model, dec, shape)
+        others["next2_trajectory"] = bench_trajectory(model, dec, shape)
         del model, dec
         torch.cuda.empty_cache()
         others["config2_attention"] = bench_attention()

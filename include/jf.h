@@ -262,6 +262,44 @@ jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t dtype,
                             jf_step_result *d_result, float *d_logits,
                             void *d_ws, jf_stream stream);
 
+/* ---- trajectories (the data collection of Jacobi Forcing) -------------------
+ * A block's Jacobi trajectory (Sec. 2.1) is the list of its iterates
+ * y^(0), ..., y^(k), stopping at the first k with y^(k) = y^(k-1); y^(k) is
+ * the fixed point.  Decoded in block mode (jf_jacobi_step mode 0, then
+ * jf_commit_kv), a block of n tokens whose first n - rows positions are
+ * accepted feeds its last `rows` tokens to a step, and the step's argmaxes
+ * give the next iterate. */
+
+/* Iterate y^(j+1) of an n-token block (Eq. 3) from y^(j) = d_prev[n] and the
+ * argmaxes d_argmax[rows] of the step that fed y^(j)'s last rows tokens
+ * (1 <= rows <= n):
+ *   d_out[i] = d_prev[i]                     for i <= n - rows
+ *   d_out[i] = d_argmax[i - (n - rows) - 1]  for i >  n - rows
+ * (accepted positions and the pending token stay; each other position takes
+ * the prediction made after its predecessor).  d_out may equal d_prev.
+ * y^(0) is the caller's initial draft.  JF_E_SHAPE unless 1 <= rows <= n. */
+jf_status jf_trajectory_record(const int32_t *d_prev, const int32_t *d_argmax,
+                               int32_t n, int32_t rows, int32_t *d_out,
+                               jf_stream stream);
+
+/* Noise-schedule point selection (App. C with the schedule of Sec. 3.1,
+ * Eq. 7).  d_traj[n_blocks][max_points][n]: block b's trajectory in its
+ * first d_len[b] points, the last of them its fixed point y*; other points
+ * are not read.  For each point, u = the number of positions that differ
+ * from y* (unconverged tokens, Sec. 3.1).  Block b's target noise ratio is
+ * t_b = (b mod w) / w (Eq. 7, blocks counted from 0), or d_t_num[b] / w
+ * when d_t_num is not NULL (any other schedule on denominator w).
+ * d_sel[b] = the point whose u / n is closest to t_b, the earliest on ties,
+ * compared exactly as |u w - t n w| in integers; -1 when d_len[b] is outside
+ * [1, max_points] (nothing of that block is read).  d_unconv (optional,
+ * [n_blocks][max_points]) receives u per point, -1 beyond d_len[b].
+ * n_blocks = 0 does nothing.  JF_E_SHAPE unless n, max_points, w >= 1. */
+jf_status jf_trajectory_select(const int32_t *d_traj, const int32_t *d_len,
+                               int32_t n_blocks, int32_t n, int32_t max_points,
+                               int32_t w, const int32_t *d_t_num,
+                               int32_t *d_sel, int32_t *d_unconv,
+                               jf_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

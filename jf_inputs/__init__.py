@@ -163,3 +163,43 @@ def model_weights(shape: dict, seed: int = 0, names=None) -> dict:
 def prompt(seed: int, length: int, vocab: int) -> np.ndarray:
     """A prompt of uniform-random token ids."""
     return token_ids(seed, 7, length, vocab)
+
+
+def trajectories(seed: int, n_blocks: int, n: int, vocab: int, max_points: int = 0,
+                 chunk: int = 1 << 16):
+    """Synthetic Jacobi trajectories of n-token blocks, shaped like the data
+    collection's: block b takes k_b uniform in [1, n] iterations, so it has
+    k_b + 1 points (int32 lengths), the last two equal to a random fixed
+    point y*.  Before them, point j keeps the first m_j = 1 + j (n-1) //
+    (k_b-1) tokens of y*, has a token different from y* at position m_j,
+    and beyond it each token is y*'s with probability 1/4 (tokens that
+    settled early), else uniform.  Returns (traj [n_blocks][max_points][n]
+    int32, with -1 in unused points; lengths [n_blocks] int32).
+    max_points defaults to n + 1."""
+    P = max_points or n + 1
+    if P < n + 1:
+        raise ValueError("max_points must be at least n + 1")
+    traj = np.full((n_blocks, P, n), -1, np.int32)
+    lengths = np.zeros(n_blocks, np.int32)
+    V = np.uint64(vocab)
+    for b0 in range(0, n_blocks, chunk):
+        B = min(chunk, n_blocks - b0)
+        k = (((_draws(stream_key(seed, 40), b0, B) >> np.uint64(32)) * np.uint64(n)) >> np.uint64(32))
+        k = k.astype(np.int64) + 1
+        lengths[b0:b0 + B] = k + 1
+        ys = (((_draws(stream_key(seed, 41), b0 * n, B * n) >> np.uint64(32)) * V) >> np.uint64(32))
+        ys = ys.astype(np.int64).reshape(B, 1, n)
+        cnt = B * P * n
+        r = _draws(stream_key(seed, 42), b0 * P * n, cnt).reshape(B, P, n)
+        rnd = ((r >> np.uint64(32)) * V >> np.uint64(32)).astype(np.int64)
+        keep = (r & np.uint64(3)) == 0
+        j = np.arange(P).reshape(1, P, 1)
+        p = np.arange(n).reshape(1, 1, n)
+        kk = k.reshape(B, 1, 1)
+        m = 1 + (j * (n - 1)) // np.maximum(kk - 1, 1)
+        off = 1 + (rnd % max(vocab - 1, 1))
+        out = np.where(p < m, ys, np.where(p == m, (ys + off) % vocab, np.where(keep, ys, rnd)))
+        out = np.where(j >= kk - 1, ys, out)
+        out = np.where(j >= kk + 1, -1, out)
+        traj[b0:b0 + B] = out.astype(np.int32)
+    return traj, lengths

@@ -719,3 +719,24 @@ extern "C" jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t 
   }
   return JF_OK;
 }
+
+// ---- trajectories ------------------------------------------------------------------------
+extern "C" jf_status jf_trajectory_record(const int32_t* d_prev, const int32_t* d_argmax, int32_t n,
+                                          int32_t rows, int32_t* d_out, jf_stream stream) {
+  if (!d_prev || !d_argmax || !d_out) return fail(JF_E_INVAL, "null pointer argument");
+  if (n < 1 || rows < 1 || rows > n) return fail(JF_E_SHAPE, "need 1 <= rows <= n (n = %d, rows = %d)", n, rows);
+  HIP_TRY(launch_traj_record(d_prev, d_argmax, n, rows, d_out, (hipStream_t)stream));
+  return JF_OK;
+}
+
+extern "C" jf_status jf_trajectory_select(const int32_t* d_traj, const int32_t* d_len, int32_t n_blocks,
+                                          int32_t n, int32_t max_points, int32_t w, const int32_t* d_t_num,
+                                          int32_t* d_sel, int32_t* d_unconv, jf_stream stream) {
+  if (!d_traj || !d_len || !d_sel) return fail(JF_E_INVAL, "null pointer argument");
+  if (n_blocks < 0 || n < 1 || max_points < 1 || w < 1)
+    return fail(JF_E_SHAPE, "need n_blocks >= 0 and n, max_points, w >= 1");
+  if (n_blocks == 0) return JF_OK;
+  HIP_TRY(launch_traj_select(d_traj, d_len, n_blocks, n, max_points, w, d_t_num, d_sel, d_unconv,
+                             (hipStream_t)stream));
+  return JF_OK;
+}

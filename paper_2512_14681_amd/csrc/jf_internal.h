@@ -159,4 +159,10 @@ hipError_t launch_fill_int(int32_t* p, int n, int32_t v, hipStream_t stream);  /
 hipError_t launch_to_f32(int dtype, const void* src, float* dst, int n, hipStream_t stream);
 hipError_t launch_copy_int(int32_t* dst, const int32_t* src, hipStream_t stream);
 
+// trajectory.hip
+hipError_t launch_traj_record(const int32_t* prev, const int32_t* g, int n, int rows, int32_t* out,
+                              hipStream_t stream);
+hipError_t launch_traj_select(const int32_t* traj, const int32_t* len, int n_blocks, int n, int max_points,
+                              int w, const int32_t* t_num, int32_t* sel, int32_t* unconv, hipStream_t stream);
+
 }  // namespace jf

@@ -11,6 +11,10 @@ paper's procedures:
 * ``generate_multiblock`` -- multi-block decoding with rejection recycling,
                             App. A Alg. 1, with the readings documented in
                             the design doc (same policy as the CPU oracle's).
+* ``collect_trajectories`` -- block-mode decoding that records every Jacobi
+                            iterate of every block on the device (the
+                            trajectories J of Sec. 2.1 that Jacobi Forcing
+                            trains on).
 """
 from __future__ import annotations
 
@@ -116,6 +120,42 @@ class Decoder:
             if mode == "block":
                 cur -= a
         return out[:max_new], accepts
+
+    # ---- Sec. 2.1 trajectories ----------------------------------------------------
+    def collect_trajectories(self, prompt, n: int, n_blocks: int, pad_seed: int = 2):
+        """Block-mode Jacobi decoding (Eq. 4) of n_blocks blocks of n tokens
+        after the prompt, recording every iterate on the device
+        (jf_trajectory_record).  y^(0) of a block is [p, pad, ...]; each step
+        feeds the block's unaccepted tail and commits the accepted rows, and
+        the block ends when its last step accepts every row it fed (then
+        y^(k) = y^(k-1)).  Returns (d_traj, lengths): d_traj is a device
+        int32 tensor [n_blocks][n + 1][n] (-1 in unused points) and block b's
+        trajectory is d_traj[b, :lengths[b]]."""
+        t, m, V = self.t, self.m, self.V
+        if n > m.cfg.max_rows:
+            raise ValueError(f"block of {n} tokens exceeds max_rows {m.cfg.max_rows}")
+        d_traj = t.full((n_blocks, n + 1, n), -1, dtype=t.int32, device="cuda")
+        lengths = np.zeros(n_blocks, np.int32)
+        p = self.prefill(prompt)
+        C = len(prompt)
+        for b in range(n_blocks):
+            self._put(self.d_tokens, [p] + [pad_token(pad_seed, C + i, V) for i in range(1, n)])
+            d_traj[b, 0].copy_(self.d_tokens[:n])
+            cur, j = n, 0
+            while cur > 0:
+                m.jf_jacobi_step(self.d_tokens, cur, 0, pad_seed, self.d_argmax, self.d_result,
+                                 self.d_tokens)
+                jf.trajectory_record(d_traj[b, j], self.d_argmax, n, cur, d_traj[b, j + 1],
+                                     stream=m.stream)
+                m.jf_commit_kv(None, self.d_result)
+                io = self.d_io[:4 + cur].cpu().numpy()
+                a = int(io[0])
+                p = int(io[4 + a - 1])
+                cur -= a
+                j += 1
+            lengths[b] = j + 1
+            C += n
+        return d_traj, lengths
 
     # ---- App. A Alg. 1 ------------------------------------------------------------
     def generate_multiblock(self, prompt, n: int, K: int, r: float, max_new: int,

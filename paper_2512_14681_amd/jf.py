@@ -94,6 +94,8 @@ _SIGS = {
     "jf_pack_matrix": (I32, [I32, I32, I32, P, P, P]),
     "jf_lm_head_ws_bytes": (SZ, [I32, I32]),
     "jf_lm_head_accept": (I32, [I32, I32, I32, I32, P, P, P, P, P, P, P, P]),
+    "jf_trajectory_record": (I32, [P, P, I32, I32, P, P]),
+    "jf_trajectory_select": (I32, [P, P, I32, I32, I32, I32, P, P, P, P]),
 }
 EXPORTS = tuple(_SIGS)
 
@@ -235,3 +237,15 @@ class Model:
         t = np.ascontiguousarray(table, dtype=np.int32)
         check(lib().jf_kv_set_page_table(self.h, t.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                          len(t), _stream(self.stream)))
+
+
+# ---- trajectories (component calls, no model) ------------------------------------
+def trajectory_record(d_prev, d_argmax, n, rows, d_out, stream=None):
+    check(lib().jf_trajectory_record(_ptr(d_prev), _ptr(d_argmax), int(n), int(rows), _ptr(d_out),
+                                     _stream(stream)))
+
+
+def trajectory_select(d_traj, d_len, n_blocks, n, max_points, w, d_sel, d_t_num=None, d_unconv=None,
+                      stream=None):
+    check(lib().jf_trajectory_select(_ptr(d_traj), _ptr(d_len), int(n_blocks), int(n), int(max_points),
+                                     int(w), _ptr(d_t_num), _ptr(d_sel), _ptr(d_unconv), _stream(stream)))
