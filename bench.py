@@ -342,15 +342,44 @@ def bench_multiblock(model, dec, shape, prefix=2048, new_tokens=64, reps=10):
     log(f"multi-block: {out}")
     return out
 
-def bench_trajectory(model, dec, shape, prefix=1024, n=16, blocks=2, sel_blocks=1 << 18, w=16,
-                     copies=4, reps=20):
+def bench_trajectory_select(n=16, sel_blocks=1 << 18, w=16, copies=4, reps=20):
+    """Noise-schedule point selection (Eq. 7, App. C) over 2^18 synthetic
+    16-token trajectories (up to 17 points each), timed over `copies`
+    rotating device copies so that no launch finds its input in the 256 MB
+    last-level cache.  Algorithmic bytes: every valid point once (L_b n 4
+    bytes per block) + the length read + the selection write (8 bytes per
+    block)."""
+    import numpy as np
+    import torch
+    import jf_inputs
+    from paper_2512_14681_amd import jf
+    t1 = time.time()
+    traj, lens = jf_inputs.trajectories(5, sel_blocks, n, 152064)
+    log(f"trajectory inputs: {time.time() - t1:.1f}s")
+    P = traj.shape[1]
+    d_src = torch.as_tensor(traj, device="cuda")
+    bufs = [d_src] + [d_src.clone() for _ in range(copies - 1)]
+    d_len = torch.as_tensor(lens, device="cuda")
+    d_sel = torch.zeros(sel_blocks, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+    call = lambda i: jf.trajectory_select(bufs[i % copies], d_len, sel_blocks, n, P, w, d_sel)
+    for i in range(copies):
+        call(i)
+    us = _time_calls(call, reps, st)
+    nbytes = int(lens.astype(np.int64).sum()) * n * 4 + 8 * sel_blocks
+    gbs = nbytes / us / 1e3
+    out = {"workload": f"noise-schedule point selection, {sel_blocks} trajectories of {n}-token blocks "
+                       f"(up to {P} points), w={w}", "blocks": sel_blocks, "n": n, "w": w, "max_points": P,
+           "mean_points": round(float(lens.mean()), 2), "us": round(us, 2), "bytes_per_launch": nbytes,
+           "GB_s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    log(f"trajectory select: {out}")
+    return out
+
+
+def bench_trajectory(model, dec, shape, prefix=1024, n=16, blocks=2):
     """Trajectory collection (Sec. 2.1) on the 7B-shaped decoder: block-mode
     decoding of `blocks` blocks of n = 16 after a 1024-token prompt with every
-    iterate recorded on the device; and the noise-schedule point selection
-    (Eq. 7, App. C) over 2^18 synthetic 16-token trajectories (up to 17
-    points each), timed over `copies` rotating device copies so that no
-    launch finds its input in the 256 MB last-level cache."""
-    import numpy as np
+    iterate recorded on the device; and the point selection."""
     import torch
     import jf_inputs
     from paper_2512_14681_amd import jf
@@ -371,31 +400,12 @@ def bench_trajectory(model, dec, shape, prefix=1024, n=16, blocks=2, sel_blocks=
     d_a, d_b = torch.zeros(n, dtype=torch.int32, device="cuda"), torch.zeros(n, dtype=torch.int32, device="cuda")
     rec_us = _time_calls(lambda i: jf.trajectory_record(d_a, d_b, n, n - (i % n), d_a), 200, st)
     collect = {"blocks": blocks, "n": n, "iterations": iters, "points_recorded": int(lengths.sum()),
-               "ms_per_iteration_wall": round(t / iters * 1e3, 3), "record_kernel_us": round(rec_us, 2),
+               "ms_per_iteration_wall": round(t / iters * 1e3, 3), "record_call_us": round(rec_us, 2),
                "note": "wall clock per iteration (prefill subtracted): step + record + commit + the "
-                       "per-iteration result read"}
-    # selection
-    t1 = time.time()
-    traj, lens = jf_inputs.trajectories(5, sel_blocks, n, V)
-    log(f"trajectory inputs: {time.time() - t1:.1f}s")
-    P = traj.shape[1]
-    d_src = torch.as_tensor(traj, device="cuda")
-    bufs = [d_src] + [d_src.clone() for _ in range(copies - 1)]
-    d_len = torch.as_tensor(lens, device="cuda")
-    d_sel = torch.zeros(sel_blocks, dtype=torch.int32, device="cuda")
-    call = lambda i: jf.trajectory_select(bufs[i % copies], d_len, sel_blocks, n, P, w, d_sel)
-    for i in range(copies):
-        call(i)
-    us = _time_calls(call, reps, st)
-    nbytes = int(lens.astype(np.int64).sum()) * n * 4 + 8 * sel_blocks
-    gbs = nbytes / us / 1e3
-    select = {"blocks": sel_blocks, "n": n, "w": w, "max_points": P, "mean_points": round(float(lens.mean()), 2),
-              "us": round(us, 2), "bytes_per_launch": nbytes, "GB_s": round(gbs, 1),
-              "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
-    del bufs, d_src
+                       "per-iteration result read; record_call_us is back-to-back calls (host-bound)"}
     out = {"workload": "trajectory collection: 7B-shaped decoder, block Jacobi n=16 after a 1024-token "
                        "prefix, every iterate recorded; point selection over 2^18 synthetic 16-token "
-                       "trajectories (Eq. 7, w=16)", "collect": collect, "select": select}
+                       "trajectories (Eq. 7, w=16)", "collect": collect, "select": bench_trajectory_select()}
     log(f"trajectory: {out}")
     return out
 
@@ -412,12 +422,14 @@ def main():
                     help="skip the per-kernel event pass (for hardware-counter runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 256 MiB device-to-device 3 times (counter calibration)")
+    ap.add_argument("--only", choices=["trajectory_select"],
+                    help="run one component workload alone and print its JSON object")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the other workloads (configs 1, 2, 3, 4 at n=32 and 64, 5)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the Jacobi step runs on a single MI355X and this "
-              "build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the Jacobi step runs on a single MI355X and the "
+              "library has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -437,6 +449,9 @@ def main():
         torch.cuda.synchronize()
         del a, b
         log(f"copy probe: 3 x {COPY_PROBE_BYTES} bytes")
+    if args.only == "trajectory_select":
+        print(json.dumps(bench_trajectory_select()), flush=True)
+        return
     shape = jf_inputs.MODEL_SHAPES["7b"]
     n, K, W = args.n, args.steps, args.warmup
     t0 = time.time()

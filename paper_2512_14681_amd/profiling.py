@@ -43,6 +43,7 @@ def _rows(directory, suffix):
 
 def short_name(name):
     """'void jf::k_gemm<unsigned short, 1, 4, 2, 1>(...)' -> 'k_gemm<bf16,1,4,2,1>'."""
+    name = name.replace("(anonymous namespace)::", "")
     name = re.sub(r"\(.*", "", name).replace("void ", "").replace("jf::", "")
     return name.replace("unsigned short", "bf16").replace(" ", "")
 
@@ -67,7 +68,7 @@ def _per_dispatch(directory, counter):
     return sorted(out)
 
 
-def traffic(fetch_dir, write_dir, kernel_regex, copy_bytes):
+def traffic(fetch_dir, write_dir, kernel_regex, copy_bytes, sources=None):
     pat = re.compile(kernel_regex)
     res = {}
     for label, directory, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
@@ -82,7 +83,7 @@ def traffic(fetch_dir, write_dir, kernel_regex, copy_bytes):
         res[label] = dict(kib=sum(vals) / len(vals), n=len(vals), copy_kib=sum(copies) / 3, scale=scale,
                           bytes=sum(vals) / len(vals) * 1024 * scale)
     digests = " ".join(f"{p}={hashlib.sha256(open(os.path.join(ROOT, p), 'rb').read()).hexdigest()}"
-                       for p in GEMM_SOURCES)
+                       for p in (sources or GEMM_SOURCES))
     f, w = res["fetch"], res["write"]
     return "\n".join([
         "| counter | dispatches | KiB per dispatch | copy probe KiB | scale (bytes per counted byte) "
@@ -111,11 +112,13 @@ def main(argv=None):
     t.add_argument("--write", required=True)
     t.add_argument("--kernel", required=True)
     t.add_argument("--copy-bytes", type=int, required=True)
+    t.add_argument("--sources", nargs="*", help="source files whose hashes the summary records "
+                   "(default: the GEMM sources)")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         print(stats(a.dir, a.top))
     else:
-        print(traffic(a.fetch, a.write, a.kernel, a.copy_bytes))
+        print(traffic(a.fetch, a.write, a.kernel, a.copy_bytes, a.sources))
 
 
 if __name__ == "__main__":
