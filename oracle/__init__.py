@@ -24,6 +24,12 @@ Contents, each citing the passage it follows:
                     App. A Alg. 1).
 * ``mock``       -- deterministic next-token backends used to drive the
                     decoding state machines without a transformer.
+* ``trajectory`` -- Jacobi trajectories of blocks (Sec. 2.1), the noise
+                    schedule (Eq. 7) and the unconverged-fraction point
+                    selection (App. C).
+* ``packed``     -- logits of a packed noisy/clean training sequence under
+                    the noise-aware and the clean-context masks (Sec. 3.1,
+                    App. C), by plain causal forwards over each chain.
 
 Precision: fp64 by default (the plain definition); a float32 mode with the
 same rounding points exists for the 7B-shaped model, whose fp64 weights would
