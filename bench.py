@@ -410,6 +410,43 @@ def bench_trajectory(model, dec, shape, prefix=1024, n=16, blocks=2):
     return out
 
 
+def bench_packed(model, dec, shape, prefix=1024, N=8, n=16, reps=10):
+    """Forward over a packed training sequence (Sec. 3.1 noise-aware causal
+    attention, App. C packing): N = 8 noisy + 8 clean blocks of n = 16
+    (R = 256 rows) after a 1024-token prompt, noise-aware mask; next to the
+    cost of the 2N separate n-row causal forwards the packing replaces."""
+    import torch
+    import jf_inputs
+    from paper_2512_14681_amd import jf
+    V = shape["vocab"]
+    dec.reset()
+    dec.prefill(jf_inputs.prompt(1, prefix, V))
+    R = 2 * N * n
+    d_tok = torch.as_tensor(jf_inputs.token_ids(8, 1, R, V), device="cuda")
+    d_arg = torch.zeros(R, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+    call = lambda i: model.jf_packed_forward(d_tok, N, n, jf.JF_MASK_NOISY_CONTEXT, d_arg)
+    for i in range(2):
+        call(i)
+    us = _time_calls(call, reps, st)
+    d_res = torch.zeros(4, dtype=torch.int32, device="cuda")
+    one = lambda i: model.jf_jacobi_step(d_tok, n, 0, 2, d_arg, d_res, d_arg)
+    for i in range(2):
+        one(i)
+    us_n = _time_calls(one, reps, st)
+    d, F, H, G, hd, Lr = (shape[k] for k in ("d_model", "d_ffn", "n_heads", "n_kv_heads", "head_dim", "n_layers"))
+    params = Lr * ((H + 2 * G) * hd * d + d * H * hd + 3 * F * d) + V * d
+    flops = 2 * params * R + Lr * 4 * R * (prefix + N * n) * hd * H
+    out = {"workload": f"packed noisy/clean forward, 7B-shaped decoder, {N}+{N} blocks of {n} "
+                       f"(R={R}) after a {prefix}-token prompt, noise-aware mask",
+           "us": round(us, 1), "rows_per_s": round(R / us * 1e6, 1),
+           "mfma_frac_bf16": round(flops / us / 1e6 / 2.5e3, 4), "tflop_s": round(flops / us / 1e6, 1),
+           "separate_forwards_us": round(2 * N * us_n, 1),
+           "note": f"separate_forwards_us = 2N x one {n}-row step ({us_n:.1f} us), the unpacked cost"}
+    log(f"packed: {out}")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -548,6 +585,7 @@ def main():
         others["config4_n64"] = bench_window(model, dec, shape, 64)
         others["config5_multiblock"] = bench_multiblock(model, dec, shape)
         others["next2_trajectory"] = bench_trajectory(model, dec, shape)
+        others["next3_packed"] = bench_packed(model, dec, shape)
         del model, dec
         torch.cuda.empty_cache()
         others["config2_attention"] = bench_attention()

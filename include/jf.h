@@ -262,6 +262,31 @@ jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t dtype,
                             jf_step_result *d_result, float *d_logits,
                             void *d_ws, jf_stream stream);
 
+/* ---- packed training sequences (forward only) -----------------------------
+ * Sec. 3.1 (noise-aware causal attention) and App. C (sequence packing): a
+ * training sequence interleaves, for each block i of a response, the noisy
+ * block selected from its trajectory and its clean fixed point, so that one
+ * forward pass gives the logits of both losses (Eq. 8 and the AR loss). */
+enum {
+  JF_MASK_NOISY_CONTEXT = 0, /* noisy block i sees the noisy blocks before it */
+  JF_MASK_CLEAN_CONTEXT = 1  /* noisy block i sees the clean blocks before it */
+};
+
+/* One forward pass over d_tokens[R], R = 2 n_blocks n (R <= max_rows), laid
+ * out [noisy_0, clean_0, noisy_1, clean_1, ...] in blocks of n, after the
+ * committed prefix (the prompt, from jf_prefill).  Every row sees the
+ * prefix and the earlier rows of its own block copy; beyond that a clean
+ * block sees the clean blocks before it, and a noisy block sees the noisy
+ * (JF_MASK_NOISY_CONTEXT) or the clean (JF_MASK_CLEAN_CONTEXT) blocks
+ * before it.  Both copies of block i sit at positions C + i n + k.
+ * Writes d_argmax[R] (lowest id on ties) and, if not NULL, the fp32 logits
+ * d_logits[R][V].  The cache slots C .. C+R-1 are overwritten and nothing
+ * is committed (a following jf_commit_kv fails with JF_E_STATE). */
+jf_status jf_packed_forward(jf_model *m, const int32_t *d_tokens,
+                            int32_t n_blocks, int32_t n, int32_t mask,
+                            int32_t *d_argmax, float *d_logits,
+                            jf_stream stream);
+
 /* ---- trajectories (the data collection of Jacobi Forcing) -------------------
  * A block's Jacobi trajectory (Sec. 2.1) is the list of its iterates
  * y^(0), ..., y^(k), stopping at the first k with y^(k) = y^(k-1); y^(k) is

@@ -349,8 +349,12 @@ extern "C" jf_status jf_profile_end(jf_model* m, double* total_ms, int32_t* laun
 // ---- forward pass of one step ---------------------------------------------------------
 // Runs rows through all layers; the K/V of row r land in cache slot C + r.
 // lm: 0 = no LM head, 1 = all rows, 2 = last row only.  g receives the argmax.
+// The rows' forest comes from sg, or from the packed layout when pk is set.
+struct PackedSpec {
+  int n_blocks, n, mask;
+};
 static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegArgs& sg, int lm,
-                         int32_t* d_g, float* d_logits, hipStream_t st) {
+                         int32_t* d_g, float* d_logits, hipStream_t st, const PackedSpec* pk = nullptr) {
   const jf_config& c = m->cfg;
   const Layout& L = m->L;
   const int dt = c.dtype;
@@ -361,8 +365,12 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
   void* xn = m->ws + L.w_xn;
   int32_t* pos = m->at<int32_t>(L.w_pos);
 
-  HIP_TRY(launch_tree(sg, R, state, m->flags(), m->at<int32_t>(L.w_parent), pos,
-                      m->at<uint64_t>(L.w_vis), st));
+  if (pk)
+    HIP_TRY(launch_tree_packed(pk->n_blocks, pk->n, pk->mask, state, m->flags(), m->at<int32_t>(L.w_parent),
+                               pos, m->at<uint64_t>(L.w_vis), st));
+  else
+    HIP_TRY(launch_tree(sg, R, state, m->flags(), m->at<int32_t>(L.w_parent), pos,
+                        m->at<uint64_t>(L.w_vis), st));
   const size_t Rp = L.Rp;
   const size_t pl_d = Rp * d, pl_h = Rp * Hhd, pl_f = Rp * F;  // activation plane strides
   // The RMSNorms are folded into the projections.  Every residual add writes
@@ -582,6 +590,33 @@ extern "C" jf_status jf_multiblock_step(jf_model* m, const int32_t* d_tokens, in
   PROF(JF_KERNEL_STEP);
   m->last_rows = R;
   m->last_tree = 1;
+  return JF_OK;
+}
+
+static_assert(kMaskNoisyContext == JF_MASK_NOISY_CONTEXT && kMaskCleanContext == JF_MASK_CLEAN_CONTEXT,
+              "mask constants");
+
+extern "C" jf_status jf_packed_forward(jf_model* m, const int32_t* d_tokens, int32_t n_blocks, int32_t n,
+                                       int32_t mask, int32_t* d_argmax, float* d_logits, jf_stream stream) {
+  if (!m || !d_tokens || !d_argmax) return fail(JF_E_INVAL, "null pointer argument");
+  if (mask != JF_MASK_NOISY_CONTEXT && mask != JF_MASK_CLEAN_CONTEXT)
+    return fail(JF_E_INVAL, "mask must be JF_MASK_NOISY_CONTEXT or JF_MASK_CLEAN_CONTEXT");
+  if (n_blocks < 1 || n < 1) return fail(JF_E_SHAPE, "need n_blocks >= 1 and n >= 1");
+  if (m->C_ub == 0) return fail(JF_E_STATE, "empty cache: prefill the prompt first");
+  if ((long long)2 * n_blocks * n > m->cfg.max_rows)
+    return fail(JF_E_CAPACITY, "2 * n_blocks * n = %lld rows exceeds max_rows %d", (long long)2 * n_blocks * n,
+                m->cfg.max_rows);
+  const int R = 2 * n_blocks * n;
+  hipStream_t st = (hipStream_t)stream;
+  jf_status s = check_rows(m, R, st);
+  if (s != JF_OK) return s;
+  const PackedSpec pk{n_blocks, n, mask};
+  SegArgs unused{};
+  PROF(JF_KERNEL_STEP);
+  s = forward(m, d_tokens, R, unused, 1, d_argmax, d_logits, st, &pk);
+  if (s != JF_OK) return s;
+  PROF(JF_KERNEL_STEP);
+  m->last_rows = 0;  // nothing to commit: the packed rows are not a draft
   return JF_OK;
 }
 

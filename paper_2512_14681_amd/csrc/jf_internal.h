@@ -107,6 +107,10 @@ struct SegArgs {
 };
 hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t* flags,
                        int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t stream);
+// the packed noisy/clean layout of a training sequence; mask as JF_MASK_* of jf.h
+constexpr int kMaskNoisyContext = 0, kMaskCleanContext = 1;
+hipError_t launch_tree_packed(int n_blocks, int n, int mask, const int32_t* state, int32_t* flags,
+                              int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t stream);
 
 // Embedding rows h[r] = E[token r] (fp32, row-major [R][d]) with the first
 // RMSNorm's input: activation planes of h * gamma in the GEMM-input layout

@@ -11,7 +11,25 @@ namespace jf {
 // ---- a1: rows of the step as a forest (Sec. 3.2, input assembly of App. A Alg. 1) ----
 // parent[r]: row whose argmax r is checked against (-1: a root, predicted by
 // the last committed row); pos[r] = C + depth(r); vis[r]: bit j set iff row j
-// is r or an ancestor of r.  One thread per row walks its own ancestor chain.
+// is r or an ancestor of r.  One thread per row walks its own ancestor chain
+// (after par[] holds every row's parent).
+__device__ void tree_walk(const int32_t* par, int r, int R, const int32_t* state, int32_t* parent,
+                          int32_t* pos, uint64_t* vis) {
+  if (r >= R) return;
+  uint64_t w[4] = {0, 0, 0, 0};
+  int depth = 0;
+  int x = r;
+  w[x >> 6] |= 1ull << (x & 63);
+  while (par[x] >= 0) {
+    x = par[x];
+    w[x >> 6] |= 1ull << (x & 63);
+    ++depth;
+  }
+  parent[r] = par[r];
+  pos[r] = state[0] + depth;
+  for (int i = 0; i < 4; ++i) vis[r * 4 + i] = w[i];
+}
+
 __global__ void k_tree(SegArgs sg, int R, const int32_t* state, int32_t* flags, int32_t* parent,
                        int32_t* pos, uint64_t* vis) {
   __shared__ int32_t par[256];
@@ -28,26 +46,49 @@ __global__ void k_tree(SegArgs sg, int R, const int32_t* state, int32_t* flags, 
     par[r] = p;
   }
   __syncthreads();
-  if (r < R) {
-    uint64_t w[4] = {0, 0, 0, 0};
-    int depth = 0;
-    int x = r;
-    w[x >> 6] |= 1ull << (x & 63);
-    while (par[x] >= 0) {
-      x = par[x];
-      w[x >> 6] |= 1ull << (x & 63);
-      ++depth;
-    }
-    parent[r] = par[r];
-    pos[r] = state[0] + depth;
-    for (int i = 0; i < 4; ++i) vis[r * 4 + i] = w[i];
-  }
+  tree_walk(par, r, R, state, parent, pos, vis);
 }
 
 hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t* flags,
                        int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t st) {
   if (R < 1 || R > 256) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_tree, dim3(1), dim3(256), 0, st, segs, R, state, flags, parent, pos, vis);
+  return hipGetLastError();
+}
+
+// Packed training sequence (Sec. 3.1 noise-aware causal attention, App. C
+// sequence packing): rows [noisy_0, clean_0, noisy_1, clean_1, ...], blocks
+// of n.  Within a block copy each row follows the previous one; the first
+// row of clean block i follows the last row of clean block i - 1, and the
+// first row of noisy block i the last row of noisy block i - 1
+// (noisy-context mask) or of clean block i - 1 (clean-context mask).  Both
+// copies of block i get depths i n .. i n + n - 1, the block's own
+// positions.
+__global__ void k_tree_packed(int n_blocks, int n, int mask, const int32_t* state, int32_t* flags,
+                              int32_t* parent, int32_t* pos, uint64_t* vis) {
+  __shared__ int32_t par[256];
+  const int R = 2 * n_blocks * n;
+  const int r = threadIdx.x;
+  if (r == 0 && flags) *flags = 0;
+  if (r < R) {
+    const int b = r / (2 * n), within = r - b * 2 * n;
+    const int copy = within / n, k = within - copy * n;   // copy 0: noisy, 1: clean
+    int p;
+    if (k > 0) p = r - 1;
+    else if (b == 0) p = -1;
+    else if (copy == 1 || mask == kMaskCleanContext) p = 2 * b * n - 1;      // last row of clean b - 1
+    else p = (2 * b - 1) * n - 1;                                            // last row of noisy b - 1
+    par[r] = p;
+  }
+  __syncthreads();
+  tree_walk(par, r, R, state, parent, pos, vis);
+}
+
+hipError_t launch_tree_packed(int n_blocks, int n, int mask, const int32_t* state, int32_t* flags,
+                              int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t st) {
+  if (n_blocks < 1 || n < 1 || 2 * n_blocks * n > 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_tree_packed, dim3(1), dim3(256), 0, st, n_blocks, n, mask, state, flags, parent, pos,
+                     vis);
   return hipGetLastError();
 }
 

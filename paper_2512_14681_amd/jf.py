@@ -21,6 +21,7 @@ JF_F32, JF_BF16 = 0, 1
 JF_ROLE_RA, JF_ROLE_CAND, JF_ROLE_PSEUDO = 0, 1, 2
 JF_MAX_SEGMENTS = 16
 JF_FLAG_BAD_TOKEN, JF_FLAG_CAPACITY = 1, 2
+JF_MASK_NOISY_CONTEXT, JF_MASK_CLEAN_CONTEXT = 0, 1
 (JF_KERNEL_QKV, JF_KERNEL_ATTN, JF_KERNEL_O, JF_KERNEL_GATEUP, JF_KERNEL_DOWN, JF_KERNEL_LMHEAD,
  JF_KERNEL_STEP) = range(1, 8)
 STATUS_NAMES = {0: "JF_OK", -1: "JF_E_INVAL", -2: "JF_E_SHAPE", -3: "JF_E_CAPACITY",
@@ -94,6 +95,7 @@ _SIGS = {
     "jf_pack_matrix": (I32, [I32, I32, I32, P, P, P]),
     "jf_lm_head_ws_bytes": (SZ, [I32, I32]),
     "jf_lm_head_accept": (I32, [I32, I32, I32, I32, P, P, P, P, P, P, P, P]),
+    "jf_packed_forward": (I32, [P, P, I32, I32, I32, P, P, P]),
     "jf_trajectory_record": (I32, [P, P, I32, I32, P, P]),
     "jf_trajectory_select": (I32, [P, P, I32, I32, I32, I32, P, P, P, P]),
 }
@@ -212,6 +214,10 @@ class Model:
         check(lib().jf_multiblock_step(self.h, _ptr(d_tokens), int(R), arr, len(segs), _ptr(d_argmax),
                                        _ptr(d_seg_accept), _ptr(d_result), _ptr(d_path),
                                        _ptr(d_logits), _stream(self.stream)))
+
+    def jf_packed_forward(self, d_tokens, n_blocks, n, mask, d_argmax, d_logits=None):
+        check(lib().jf_packed_forward(self.h, _ptr(d_tokens), int(n_blocks), int(n), int(mask),
+                                      _ptr(d_argmax), _ptr(d_logits), _stream(self.stream)))
 
     def jf_commit_kv(self, d_path, d_result, max_commit=0):
         check(lib().jf_commit_kv(self.h, _ptr(d_path), _ptr(d_result), int(max_commit),
