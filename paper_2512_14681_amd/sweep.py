@@ -18,6 +18,13 @@ On the 7B-shaped bf16 decoder (random-init weights, a random prompt):
   each iteration accepts k tokens.  Tokens/s at each k are reported next to
   the one-row (autoregressive) rate.
 
+* with --grid, the configuration grid of App. E on latency only: block size
+  n x verification size v (entries verified in parallel, each n tokens) at
+  K = 2 blocks; one step holds the real-active draft, v - 1 recycled
+  n-token entries under its root and one pseudo-active block,
+  R = (v + 1) n rows.  Points beyond the engine's 256 rows are reported as
+  such.  Tokens/s needs the TPF of trained weights and is not reported.
+
 Prints one JSON object (stdout); progress on stderr.
 """
 from __future__ import annotations
@@ -39,6 +46,9 @@ def main(argv=None):
     ap.add_argument("--cands", default="0,1,2,4,6,8,10,12,15")
     ap.add_argument("--k", default="1,2,3,4,5,8")
     ap.add_argument("--reps", type=int, default=10)
+    ap.add_argument("--grid", action="store_true", help="the (n, verification size) grid at K = 2")
+    ap.add_argument("--grid-n", default="8,16,32,64,128")
+    ap.add_argument("--grid-v", default="1,2,4,8,12")
     args = ap.parse_args(argv)
 
     import numpy as np
@@ -104,6 +114,26 @@ def main(argv=None):
         tree.append(dict(costs(R, us), candidates=c))
         log(f"tree R={R}: {us:.1f} us")
 
+    grid = []
+    if args.grid:
+        for n_ in (int(x) for x in args.grid_n.split(",")):
+            for v in (int(x) for x in args.grid_v.split(",")):
+                R = (v + 1) * n_
+                if R > Rmax:
+                    grid.append({"n": n_, "v": v, "rows": R, "us": None, "note": "exceeds 256 rows"})
+                    continue
+                segs = [(0, n_, -1, jf.JF_ROLE_RA, 1)]
+                for c in range(v - 1):
+                    segs.append((n_ * (1 + c), n_, 0, jf.JF_ROLE_CAND, 0))
+                segs.append((n_ * v, n_, n_ - 1, jf.JF_ROLE_PSEUDO, 0))
+                if len(segs) > jf.JF_MAX_SEGMENTS:
+                    grid.append({"n": n_, "v": v, "rows": R, "us": None, "note": "more than 16 segments"})
+                    continue
+                us = timed(lambda: model.jf_multiblock_step(d_tok, R, segs, d_arg, d_seg, d_res, d_path),
+                           args.reps)
+                grid.append(dict(costs(R, us), n=n_, v=v))
+                log(f"grid n={n_} v={v} R={R}: {us:.1f} us")
+
     # fixed fast-forward emulation
     ks = [int(k) for k in args.k.split(",")]
     n, iters = 16, 12
@@ -141,7 +171,7 @@ def main(argv=None):
         for f in fixed:
             f["speedup_vs_one_row_steps"] = round(f["tokens_s"] / (1e6 / ar_us), 3)
     out = {"workload": f"7B-shaped bf16 decoder, {P}-token prefix, random-init weights",
-           "linear": linear, "tree": tree, "fixed_tpf_block16": fixed,
+           "linear": linear, "tree": tree, "fixed_tpf_block16": fixed, "config_grid_k2": grid,
            "note": f"one-row step {ar_us} us; C0 after greedy continuation {C0}"}
     print(json.dumps(out), flush=True)
 
