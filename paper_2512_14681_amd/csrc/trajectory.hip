@@ -161,8 +161,9 @@ __global__ void __launch_bounds__(256) k_traj_select_multi(const int32_t* __rest
     __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int32_t*>(traj + (size_t)(b0 + i) * max_points * n), 0, valid, kBufferFlags);
 #pragma unroll
-    for (int q = 0; q < K; ++q) v[i][q] = __builtin_amdgcn_raw_buffer_load_b32(rs, lane * 4, q * per * n * 4, 0);
-    ys[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, pos * 4, (L - 1) * n * 4, 0);
+    // whole offsets in the vector operand, the range-checked one
+    for (int q = 0; q < K; ++q) v[i][q] = __builtin_amdgcn_raw_buffer_load_b32(rs, (q * per * n + lane) * 4, 0, 0);
+    ys[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, ((L - 1) * n + pos) * 4, 0, 0);
   }
   // this lane's own point (j = lane): load lq, slice lsl
   const int lq = lane / per;
