@@ -94,3 +94,34 @@ def packed_logits(model, prompt, noisy, clean, mask: int):
     else:
         raise ValueError("mask must be NOISY_CONTEXT or CLEAN_CONTEXT")
     return out
+
+
+def packed_logits_after_prefix(model, noisy, clean, mask: int):
+    """packed_logits with the prompt already committed in the model's cache
+    (length P): the chains are run after it, and the cache is cut back to P
+    after each.  The same definition, without recomputing the prompt."""
+    P = model.length
+    N, n = len(noisy), len(noisy[0])
+
+    def chain(blocks):
+        toks = np.asarray(sum(([int(t) for t in b] for b in blocks), []))
+        T = len(toks)
+        z, _ = model.forward(toks, P + np.arange(T), np.tri(T, dtype=bool))
+        model.truncate(P)
+        return z
+
+    zc = chain(clean)
+    out = np.zeros((2 * N * n, zc.shape[1]), zc.dtype)
+    for i in range(N):
+        out[row_of(i, 1, 0, n):row_of(i, 1, 0, n) + n] = zc[i * n:(i + 1) * n]
+    if mask == NOISY_CONTEXT:
+        zn = chain(noisy)
+        for i in range(N):
+            out[row_of(i, 0, 0, n):row_of(i, 0, 0, n) + n] = zn[i * n:(i + 1) * n]
+    elif mask == CLEAN_CONTEXT:
+        for i in range(N):
+            z = chain(list(clean[:i]) + [noisy[i]])
+            out[row_of(i, 0, 0, n):row_of(i, 0, 0, n) + n] = z[i * n:(i + 1) * n]
+    else:
+        raise ValueError("mask must be NOISY_CONTEXT or CLEAN_CONTEXT")
+    return out

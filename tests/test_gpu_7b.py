@@ -12,6 +12,11 @@ benchmark times.
   real-active draft, 3 pseudo-active blocks and 8 candidate n-grams of 16
   rows (R = 192) under the tree mask; one candidate holds the oracle's greedy
   continuation and must win.
+* The packed noisy/clean forward as benchmarked: 8 noisy + 8 clean blocks of
+  16 (256 rows) after the 1024-token prompt, noise-aware mask, every row.
+* Trajectory recording as benchmarked (a block of 16 after the 1024-token
+  prompt), teacher-forced: each recorded iterate's successor is the
+  oracle's Eq. 3 update of it.
 
 The oracle runs in float32 with the bf16 K/V rounding points of the model
 (batched attention; fp32 weights cached: ~30 GB of host memory).  Bar (bf16):
@@ -25,6 +30,7 @@ import pytest
 
 import jf_inputs
 from oracle import jacobi as ojac
+from oracle import packed as opk
 from oracle import tree as otree
 from oracle.model import DecoderOracle
 
@@ -184,3 +190,53 @@ def test_7b_multiblock_step_r192(env):
         assert res[1] == win and res[0] == len(path)
         assert list(d_path.cpu().numpy()[:len(path)]) == list(path)
     assert win == 7 and len(path) >= 9          # candidate 3 (segment 4 + 3) holds the greedy tokens
+
+
+def test_7b_packed_forward_256_rows(env, prompt1024):
+    """The packed forward as benchmarked: 8 + 8 blocks of 16 after the
+    1024-token prompt, noise-aware mask; all 256 rows against the oracle's
+    two chains."""
+    import torch
+    from paper_2512_14681_amd import jf
+    dec, model = env["dec"], env["model"]
+    N, n = 8, 16
+    noisy = [list(jf_inputs.token_ids(8, 2 * i, n, V)) for i in range(N)]
+    clean = [list(jf_inputs.token_ids(8, 2 * i + 1, n, V)) for i in range(N)]
+    dec.reset()
+    dec.prefill(prompt1024)
+    R = 2 * N * n
+    d_tok = torch.tensor(opk.packed_tokens(noisy, clean), dtype=torch.int32, device="cuda")
+    d_arg = torch.zeros(R, dtype=torch.int32, device="cuda")
+    d_log = torch.empty((R, V), dtype=torch.float32, device="cuda")
+    model.jf_packed_forward(d_tok, N, n, jf.JF_MASK_NOISY_CONTEXT, d_arg, d_log)
+    z = d_log.cpu().numpy()
+    g = d_arg.cpu().numpy()
+    oracle_prefix(env, prompt1024)
+    zo = opk.packed_logits_after_prefix(env["ora"], noisy, clean, opk.NOISY_CONTEXT)
+    err = np.abs(z - zo).max()
+    say(f"packed forward R={R}: max |logit - oracle| = {err:.2e}")
+    assert err < LOGIT_TOL, err
+    assert ((g == zo.argmax(1)) | (gap(zo) < GAP_EXEMPT)).all()
+
+
+def test_7b_trajectory_teacher_forced(env, prompt1024):
+    """One block of 16 recorded on the GPU: y^(0) = [p, pad ...], and every
+    y^(j+1) is the oracle's Eq. 3 update of the GPU's y^(j) (the oracle's
+    greedy prediction after each prefix of y^(j)), up to near-ties."""
+    dec = env["dec"]
+    n = 16
+    dec.reset()
+    d_traj, lengths = dec.collect_trajectories(prompt1024, n, 1)
+    traj = d_traj.cpu().numpy()[0, :lengths[0]]
+    say(f"trajectory: {lengths[0]} points")
+    assert 2 <= lengths[0] <= n + 1
+    assert (traj[-1] == traj[-2]).all()
+    last = oracle_prefix(env, prompt1024)
+    assert traj[0][0] == int(last.argmax()) or gap(last) < GAP_EXEMPT
+    assert traj[0][1:].tolist() == [ojac.pad_id(2, 1024 + i, V) for i in range(1, n)]
+    ora = env["ora"]
+    for j in range(lengths[0] - 1):
+        zo, _ = ora.forward(traj[j], 1024 + np.arange(n), np.tri(n, dtype=bool))
+        want = np.concatenate([[traj[j][0]], zo.argmax(1)[:n - 1]])
+        ok = (traj[j + 1] == want) | np.concatenate([[True], gap(zo)[:n - 1] < GAP_EXEMPT])
+        assert ok.all(), (j, np.nonzero(~ok))

@@ -81,3 +81,18 @@ def test_masks_agree_where_the_contexts_do(tiny):
     a2 = opk.packed_logits(m, prompt, noisy2, clean, opk.NOISY_CONTEXT)
     b2 = opk.packed_logits(m, prompt, noisy2, clean, opk.CLEAN_CONTEXT)
     assert np.abs(a2 - b2).max() < 1e-12
+
+
+@pytest.mark.parametrize("mask", [opk.NOISY_CONTEXT, opk.CLEAN_CONTEXT])
+def test_after_prefix_form_equals_the_full_form(tiny, mask):
+    w, m = tiny
+    prompt = jf_inputs.prompt(8, 18, SHAPE["vocab"])
+    N, n, V = 3, 4, SHAPE["vocab"]
+    clean = [list(jf_inputs.token_ids(9, i, n, V)) for i in range(N)]
+    noisy = [list(jf_inputs.token_ids(10, i, n, V)) for i in range(N)]
+    full = opk.packed_logits(m, prompt, noisy, clean, mask)
+    m2 = DecoderOracle(SHAPE, w)
+    m2.prefill(np.asarray(prompt))
+    cached = opk.packed_logits_after_prefix(m2, noisy, clean, mask)
+    assert m2.length == len(prompt)
+    assert np.abs(full - cached).max() < 1e-10
