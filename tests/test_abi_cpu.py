@@ -90,6 +90,16 @@ def test_null_arguments_rejected_without_hip(L):
     assert L.jf_pack_matrix(20, 128, 1, P(1), P(1), None) == jf.JF_E_SHAPE
     assert L.jf_lm_head_accept(4, 100, 1024, 1, P(1), P(1), None, P(1), None, None, P(1), None) == jf.JF_E_SHAPE
     assert L.jf_lm_head_accept(4, 128, 1024, 1, P(1), P(1), P(1), P(1), None, None, P(1), None) == jf.JF_E_INVAL
+    # packed forward and trajectories: argument checks happen before any HIP call
+    assert L.jf_packed_forward(None, P(1), 2, 8, 0, P(1), None, None) == jf.JF_E_INVAL
+    assert L.jf_trajectory_record(None, P(1), 16, 4, P(1), None) == jf.JF_E_INVAL
+    assert L.jf_trajectory_record(P(1), P(1), 16, 17, P(1), None) == jf.JF_E_SHAPE
+    assert L.jf_trajectory_record(P(1), P(1), 16, 0, P(1), None) == jf.JF_E_SHAPE
+    assert L.jf_trajectory_select(P(1), None, 4, 16, 17, 16, None, P(1), None, None) == jf.JF_E_INVAL
+    assert L.jf_trajectory_select(P(1), P(1), 4, 0, 17, 16, None, P(1), None, None) == jf.JF_E_SHAPE
+    assert L.jf_trajectory_select(P(1), P(1), 4, 16, 17, 0, None, P(1), None, None) == jf.JF_E_SHAPE
+    assert L.jf_trajectory_select(P(1), P(1), -1, 16, 17, 16, None, P(1), None, None) == jf.JF_E_SHAPE
+    assert L.jf_trajectory_select(P(1), P(1), 0, 16, 17, 16, None, P(1), None, None) == jf.JF_OK
 
 
 def test_last_error_is_thread_local(L):
