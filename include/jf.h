@@ -315,7 +315,8 @@ jf_status jf_trajectory_record(const int32_t *d_prev, const int32_t *d_argmax,
  * t_b = (b mod w) / w (Eq. 7, blocks counted from 0), or d_t_num[b] / w
  * when d_t_num is not NULL (any other schedule on denominator w).
  * d_sel[b] = the point whose u / n is closest to t_b, the earliest on ties,
- * compared exactly as |u w - t n w| in integers; -1 when d_len[b] is outside
+ * compared exactly in integers as |u w - t_num n| (t_num = b mod w or
+ * d_t_num[b]); -1 when d_len[b] is outside
  * [1, max_points] (nothing of that block is read).  d_unconv (optional,
  * [n_blocks][max_points]) receives u per point, -1 beyond d_len[b].
  * n_blocks = 0 does nothing.  JF_E_SHAPE unless n, max_points, w >= 1. */
