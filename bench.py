@@ -283,7 +283,32 @@ def bench_window(model, dec, shape, n, prompt_len=1024, steps=10, warmup=3):
     return out
 
 
-def bench_multiblock(model, dec, shape, prefix=2048, new_tokens=64, reps=10):
+def bench_decode(model, dec, shape, n, new_tokens=256, prompt_len=1024):
+    """Greedy Jacobi decoding, running window of n, 256 new tokens after a
+    1024-token prompt: wall clock per iteration (prefill subtracted),
+    including the host loop and its per-iteration result read."""
+    import torch
+    import jf_inputs
+    V = shape["vocab"]
+    prompt = jf_inputs.prompt(1, prompt_len, V)
+    dec.reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    dec.prefill(prompt)
+    t_prefill = time.perf_counter() - t0
+    dec.reset()
+    t0 = time.perf_counter()
+    toks, acc = dec.generate_jacobi(prompt, n, new_tokens, mode="window", pad_seed=2)
+    t = time.perf_counter() - t0 - t_prefill
+    out = {"workload": f"7B-shaped decoder, greedy Jacobi decoding, n={n} running window, {new_tokens} new "
+                       f"tokens after a {prompt_len}-token prompt",
+           "new_tokens": len(toks), "iterations": len(acc), "tpf": round(len(toks) / len(acc), 3),
+           "ms_per_iteration_wall": round(t / len(acc) * 1e3, 3), "tokens_s_wall": round(len(toks) / t, 1)}
+    log(f"decode n={n}: {out}")
+    return out
+
+
+def bench_multiblock(model, dec, shape, prefix=2048, new_tokens=256, reps=10):
     """Multi-block decoding with rejection recycling (K = 4 blocks of n = 16,
     r = 0.85, up to 8 recycled 16-token candidates) after a 2048-token
     prompt; and the largest step of that configuration, R = 192 rows (the
@@ -583,6 +608,8 @@ def main():
         others = {}
         others["config4_n32"] = bench_window(model, dec, shape, 32)
         others["config4_n64"] = bench_window(model, dec, shape, 64)
+        others["config4_decode_n16"] = bench_decode(model, dec, shape, 16)
+        others["config4_decode_n32"] = bench_decode(model, dec, shape, 32)
         others["config5_multiblock"] = bench_multiblock(model, dec, shape)
         others["next2_trajectory"] = bench_trajectory(model, dec, shape)
         others["next3_packed"] = bench_packed(model, dec, shape)
