@@ -192,10 +192,11 @@ def test_7b_multiblock_step_r192(env):
     assert win == 7 and len(path) >= 9          # candidate 3 (segment 4 + 3) holds the greedy tokens
 
 
-def test_7b_packed_forward_256_rows(env, prompt1024):
+@pytest.mark.parametrize("mask", [opk.NOISY_CONTEXT, opk.CLEAN_CONTEXT])
+def test_7b_packed_forward_256_rows(env, prompt1024, mask):
     """The packed forward as benchmarked: 8 + 8 blocks of 16 after the
-    1024-token prompt, noise-aware mask; all 256 rows against the oracle's
-    two chains."""
+    1024-token prompt; all 256 rows against the oracle's chains, under the
+    noise-aware mask (benchmarked) and the clean-context one."""
     import torch
     from paper_2512_14681_amd import jf
     dec, model = env["dec"], env["model"]
@@ -208,13 +209,13 @@ def test_7b_packed_forward_256_rows(env, prompt1024):
     d_tok = torch.tensor(opk.packed_tokens(noisy, clean), dtype=torch.int32, device="cuda")
     d_arg = torch.zeros(R, dtype=torch.int32, device="cuda")
     d_log = torch.empty((R, V), dtype=torch.float32, device="cuda")
-    model.jf_packed_forward(d_tok, N, n, jf.JF_MASK_NOISY_CONTEXT, d_arg, d_log)
+    model.jf_packed_forward(d_tok, N, n, mask, d_arg, d_log)
     z = d_log.cpu().numpy()
     g = d_arg.cpu().numpy()
     oracle_prefix(env, prompt1024)
-    zo = opk.packed_logits_after_prefix(env["ora"], noisy, clean, opk.NOISY_CONTEXT)
+    zo = opk.packed_logits_after_prefix(env["ora"], noisy, clean, mask)
     err = np.abs(z - zo).max()
-    say(f"packed forward R={R}: max |logit - oracle| = {err:.2e}")
+    say(f"packed forward R={R} mask={mask}: max |logit - oracle| = {err:.2e}")
     assert err < LOGIT_TOL, err
     assert ((g == zo.argmax(1)) | (gap(zo) < GAP_EXEMPT)).all()
 
