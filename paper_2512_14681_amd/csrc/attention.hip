@@ -71,7 +71,13 @@ __device__ __forceinline__ uint32_t low_bits8(int n) {
   return n >= 8 ? 0xFFu : (n <= 0 ? 0u : (1u << n) - 1u);
 }
 
-template <typename T, int HD>
+// QT query tiles per block (QT = 1, or 2 for many query tiles over long
+// prefixes, see attn_plan): each key chunk's K and V^T fragments, loaded
+// once, serve all QT tiles of the wave, so the keys are read once per QT
+// tiles.  With QT = 2 one chunk is in
+// flight per wave instead of two (the register budget of two blocks per
+// CU), and the waves' states merge tile after tile.
+template <typename T, int HD, int QT>
 __global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
   constexpr int NW = 4;  // waves per block
   __shared__ float s_m[NW][16], s_l[NW][16];
@@ -79,7 +85,7 @@ __global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
   __shared__ float s_f[NW][16], s_M[16], s_den[16];
   __shared__ int s_pt[kAttnMaxPages];
   const int g = blockIdx.x;
-  const int tile = blockIdx.y;
+  const int tile0 = blockIdx.y * QT;
   const int split = blockIdx.z, S = gridDim.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = a.H / a.G;
@@ -98,39 +104,45 @@ __global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
   const int lim = min(k1, C + R);                 // keys at or past lim are not visible here
 
   const int ql = lane & 15, kg = lane >> 4;
-  const int qr = tile * 16 + ql;
-  const bool qvalid = qr < nq;
-  const int hl = qvalid ? qr / R : 0;
-  const int r = qvalid ? qr - hl * R : 0;
-  const int head = g * grp + hl;
-
   const T* kv = reinterpret_cast<const T*>(a.kv);
   const size_t page_elems = (size_t)2 * a.G * kPage * HD;
   const size_t k_off = (size_t)g * kPage * HD;
   const size_t vt_off = (size_t)a.G * kPage * HD + (size_t)g * HD * kPage;
 
-  ActFrag<T> qf[HD / 32];
-  const T* qp = reinterpret_cast<const T*>(a.q) + ((size_t)r * a.H + head) * HD + 8 * kg;
+  ActFrag<T> qf[QT][HD / 32];
+  uint64_t vw[QT][4];
 #pragma unroll
-  for (int c = 0; c < HD / 32; ++c) qf[c] = qvalid ? act_load<T>(qp + 32 * c, a.q_plane) : act_zero<T>();
-
-  uint64_t vw[4];
+  for (int t = 0; t < QT; ++t) {
+    const int qr = (tile0 + t) * 16 + ql;
+    const bool qvalid = qr < nq;
+    const int hl = qvalid ? qr / R : 0;
+    const int r = qvalid ? qr - hl * R : 0;
+    const int head = g * grp + hl;
+    const T* qp = reinterpret_cast<const T*>(a.q) + ((size_t)r * a.H + head) * HD + 8 * kg;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (a.vis) {
-      vw[i] = a.vis[r * 4 + i];
-    } else {  // causal: rows 0..r
-      int lo = i * 64;
-      vw[i] = r < lo ? 0ull : (r - lo >= 63 ? ~0ull : ((2ull << (r - lo)) - 1ull));
+    for (int c = 0; c < HD / 32; ++c) qf[t][c] = qvalid ? act_load<T>(qp + 32 * c, a.q_plane) : act_zero<T>();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (a.vis) {
+        vw[t][i] = a.vis[r * 4 + i];
+      } else {  // causal: rows 0..r
+        int lo = i * 64;
+        vw[t][i] = r < lo ? 0ull : (r - lo >= 63 ? ~0ull : ((2ull << (r - lo)) - 1ull));
+      }
     }
   }
   __syncthreads();  // s_pt
 
   const float scale = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t o[HD / 16];
+  float m_run[QT], l_run[QT];
+  f32x4_t o[QT][HD / 16];
 #pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) o[t][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
 
   // One 32-key chunk (inside one page): K rows of the two score tiles, row i
   // of tile kt being key 8 (i / 4) + 4 kt + i % 4, and the V^T fragments
@@ -151,129 +163,149 @@ __global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
   };
   auto compute = [&](int c, const Frag<T> (&kf)[2][HD / 32], const Frag<T> (&vf)[HD / 16]) {
     const int key0 = k0 + 32 * c + 8 * kg;  // key of p[0]; p[e] is key0 + e
-    f32x4_t sc[2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      if constexpr (sizeof(T) == 2) {
-        // Q = hi + lo: four independent accumulation chains
-        f32x4_t sh = f32x4_t{0.f, 0.f, 0.f, 0.f}, sl = sh;
+    for (int t = 0; t < QT; ++t) {
+      f32x4_t sc[2];
 #pragma unroll
-        for (int cc = 0; cc < HD / 32; ++cc) {
-          mfma(sh, kf[kt][cc], qf[cc].hi);
-          mfma(sl, kf[kt][cc], qf[cc].lo);
+      for (int kt = 0; kt < 2; ++kt) {
+        if constexpr (sizeof(T) == 2) {
+          // Q = hi + lo: four independent accumulation chains
+          f32x4_t sh = f32x4_t{0.f, 0.f, 0.f, 0.f}, sl = sh;
+#pragma unroll
+          for (int cc = 0; cc < HD / 32; ++cc) {
+            mfma(sh, kf[kt][cc], qf[t][cc].hi);
+            mfma(sl, kf[kt][cc], qf[t][cc].lo);
+          }
+          sc[kt] = sh + sl;
+        } else {
+          sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int cc = 0; cc < HD / 32; ++cc) mfma(sc[kt], kf[kt][cc], qf[t][cc]);
         }
-        sc[kt] = sh + sl;
+      }
+      // visible: below lim, and either in the prefix or marked in the row's mask
+      const uint32_t vis = low_bits8(lim - key0) & (low_bits8(C - key0) | vis_bits8(vw[t], key0 - C));
+      float p[8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = kt * 4 + i;
+          const float v = ((vis >> e) & 1u) ? sc[kt][i] * scale : -INFINITY;
+          p[e] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run[t], mx);
+      // No branch: the MFMAs need every lane.  A query with nothing visible
+      // yet keeps p = 0 and m = -inf.
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      // exponents are <= 0 (or -inf): the bare hardware exp2 suffices
+      const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_use);
+      float psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(p[e] - m_use);
+        psum += p[e];
+      }
+      l_run[t] = l_run[t] * alpha + psum;
+      m_run[t] = m_new;
+      const PFrag<T> pf = pfrag<T>(p);
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt) o[t][dt] *= alpha;
+      if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) mfma(o[t][dt], vf[dt], pf.hi);
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) mfma(o[t][dt], vf[dt], pf.lo);
       } else {
-        sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int cc = 0; cc < HD / 32; ++cc) mfma(sc[kt], kf[kt][cc], qf[cc]);
+        for (int dt = 0; dt < HD / 16; ++dt) mfma(o[t][dt], vf[dt], pf.v);
       }
-    }
-    // visible: below lim, and either in the prefix or marked in the row's mask
-    const uint32_t vis = low_bits8(lim - key0) & (low_bits8(C - key0) | vis_bits8(vw, key0 - C));
-    float p[8];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = kt * 4 + i;
-        const float v = ((vis >> e) & 1u) ? sc[kt][i] * scale : -INFINITY;
-        p[e] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    // No branch: the MFMAs need every lane.  A query with nothing visible
-    // yet keeps p = 0 and m = -inf.
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    // exponents are <= 0 (or -inf): the bare hardware exp2 suffices
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float psum = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      p[e] = __builtin_amdgcn_exp2f(p[e] - m_use);
-      psum += p[e];
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    const PFrag<T> pf = pfrag<T>(p);
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) o[dt] *= alpha;
-    if constexpr (sizeof(T) == 2) {
-#pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.hi);
-#pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.lo);
-    } else {
-#pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.v);
     }
   };
 
-  // Chunks wave, wave + NW, ... (mine of them), two at a time: both loads
-  // are issued (unconditionally; past the end they re-read the last chunk,
-  // unused), then both chunks are consumed.  The launch plan gives each
-  // wave at most two chunks, i.e. one memory round trip.
-  Frag<T> kA[2][HD / 32], kB[2][HD / 32];
-  Frag<T> vA[HD / 16], vB[HD / 16];
+  // Chunks wave, wave + NW, ... (mine of them).  QT = 1: two at a time, both
+  // loads issued (unconditionally; past the end they re-read the last
+  // chunk, unused), then both chunks consumed; the launch plan gives each
+  // wave at most two chunks, i.e. one memory round trip.  QT = 2: one at a
+  // time.
   const int mine = wave < nch ? (nch - wave + NW - 1) / NW : 0;
-  for (int i = 0; i < mine; i += 2) {
-    const int cA = wave + i * NW, cB = min(cA + NW, nch - 1);
-    load(cA, kA, vA);
-    load(cB, kB, vB);
-    compute(cA, kA, vA);
-    if (i + 1 < mine) compute(cA + NW, kB, vB);
-  }
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
-
-  // Merge the waves' partial softmax states in LDS: per query row the
-  // waves' weights 2^(m_w - M) and the sum once, then every element.
-  if (kg == 0) {
-    s_m[wave][ql] = m_run;
-    s_l[wave][ql] = l_run;
-  }
-#pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) s_o[wave][ql][dt * 16 + 4 * kg + i] = o[dt][i];
-  __syncthreads();
-  if (threadIdx.x < 16) {
-    const int q = threadIdx.x;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][q]);
-    float den = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float f = s_m[w][q] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[w][q] - M);
-      s_f[w][q] = f;
-      den += s_l[w][q] * f;
+  if constexpr (QT == 1) {
+    Frag<T> kA[2][HD / 32], kB[2][HD / 32];
+    Frag<T> vA[HD / 16], vB[HD / 16];
+    for (int i = 0; i < mine; i += 2) {
+      const int cA = wave + i * NW, cB = min(cA + NW, nch - 1);
+      load(cA, kA, vA);
+      load(cB, kB, vB);
+      compute(cA, kA, vA);
+      if (i + 1 < mine) compute(cA + NW, kB, vB);
     }
-    s_M[q] = M;
-    s_den[q] = den;
+  } else {
+    Frag<T> kA[2][HD / 32];
+    Frag<T> vA[HD / 16];
+    for (int i = 0; i < mine; ++i) {
+      const int c = wave + i * NW;
+      load(c, kA, vA);
+      compute(c, kA, vA);
+    }
   }
-  __syncthreads();
+
+  // Merge the waves' partial softmax states in LDS, one query tile at a
+  // time: per query row the waves' weights 2^(m_w - M) and the sum once,
+  // then every element.
   const size_t nrow = (size_t)R * a.H;
-  for (int e = threadIdx.x; e < 16 * HD; e += 64 * NW) {
-    const int q = e / HD, dim = e - q * HD;
-    const int qq = tile * 16 + q;
-    if (qq >= nq) continue;
-    float num = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) num += s_o[w][q][dim] * s_f[w][q];
-    const int hq = qq / R, rr = qq - hq * R;
-    if (S == 1) {
-      act_store<T>(reinterpret_cast<T*>(a.out) + act_offset(rr, (g * grp + hq) * HD + dim, a.H * HD), a.out_plane,
-                   num / s_den[q]);
-    } else {
-      const size_t qidx = (size_t)rr * a.H + g * grp + hq;
-      a.o_part[((size_t)split * nrow + qidx) * HD + dim] = num;
-      if (dim == 0) {
-        a.ml_part[((size_t)split * nrow + qidx) * 2 + 0] = s_M[q];
-        a.ml_part[((size_t)split * nrow + qidx) * 2 + 1] = s_den[q];
+  for (int t = 0; t < QT; ++t) {
+    float lr = l_run[t];
+    lr += __shfl_xor(lr, 16);
+    lr += __shfl_xor(lr, 32);
+    if (t > 0) __syncthreads();  // the previous tile's reads of s_o are done
+    if (kg == 0) {
+      s_m[wave][ql] = m_run[t];
+      s_l[wave][ql] = lr;
+    }
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s_o[wave][ql][dt * 16 + 4 * kg + i] = o[t][dt][i];
+    __syncthreads();
+    if (threadIdx.x < 16) {
+      const int q = threadIdx.x;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][q]);
+      float den = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float f = s_m[w][q] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[w][q] - M);
+        s_f[w][q] = f;
+        den += s_l[w][q] * f;
+      }
+      s_M[q] = M;
+      s_den[q] = den;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < 16 * HD; e += 64 * NW) {
+      const int q = e / HD, dim = e - q * HD;
+      const int qq = (tile0 + t) * 16 + q;
+      if (qq >= nq) continue;
+      float num = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) num += s_o[w][q][dim] * s_f[w][q];
+      const int hq = qq / R, rr = qq - hq * R;
+      if (S == 1) {
+        act_store<T>(reinterpret_cast<T*>(a.out) + act_offset(rr, (g * grp + hq) * HD + dim, a.H * HD),
+                     a.out_plane, num / s_den[q]);
+      } else {
+        const size_t qidx = (size_t)rr * a.H + g * grp + hq;
+        a.o_part[((size_t)split * nrow + qidx) * HD + dim] = num;
+        if (dim == 0) {
+          a.ml_part[((size_t)split * nrow + qidx) * 2 + 0] = s_M[q];
+          a.ml_part[((size_t)split * nrow + qidx) * 2 + 1] = s_den[q];
+        }
       }
     }
   }
@@ -322,6 +354,13 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 // Launch shape: key splits such that each of a block's 4 waves gets at most
 // kAttnChunksPerWave 32-key chunks (one memory round trip), at most
 // kAttnMaxSplits splits, and at most kAttnMaxPages - 2 pages per split.
+// Two query tiles per block from this many (query tiles x keys) on: measured
+// on the attention workloads (28 q / 4 kv heads of 128), two tiles won at
+// 57k and more (P = 8192, n = 16: -17%; P = 2048, n = 64: -15%) and lost at
+// 29k (P = 2048, n = 32: +5%), where the one-chunk-in-flight loop costs more
+// than the halved key traffic saves.
+constexpr long kAttnQt2Work = 50000;
+
 void attn_plan(AttnArgs& a) {
   const int chunks = (a.keys_ub + 31) / 32;
   a.waves = 4;
@@ -329,13 +368,20 @@ void attn_plan(AttnArgs& a) {
   const int min_s = (a.keys_ub + (kAttnMaxPages - 2) * kPage - 1) / ((kAttnMaxPages - 2) * kPage);
   if (s < min_s) s = min_s;
   a.splits = s < 1 ? 1 : (s > kAttnMaxSplits ? kAttnMaxSplits : s);
+  // Many query tiles over long prefixes: two query tiles per block share
+  // each key chunk.
+  const long qtiles = ((long)(a.H / a.G) * a.R + 15) / 16;
+  a.qt = qtiles >= 2 && qtiles * a.keys_ub >= kAttnQt2Work ? 2 : 1;
 }
 
 template <typename T, int HD>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const int nq = (a.H / a.G) * a.R;
   const int ntiles = (nq + 15) / 16;
-  hipLaunchKernelGGL((k_attn<T, HD>), dim3(a.G, ntiles, a.splits), dim3(256), 0, st, a);
+  if (a.qt == 2)
+    hipLaunchKernelGGL((k_attn<T, HD, 2>), dim3(a.G, (ntiles + 1) / 2, a.splits), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_attn<T, HD, 1>), dim3(a.G, ntiles, a.splits), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   const dim3 grid(a.G, ntiles, HD / 32);

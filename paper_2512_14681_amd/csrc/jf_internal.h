@@ -127,6 +127,7 @@ struct AttnArgs {
   int H, G, hd, R, max_ctx;
   int splits;
   int waves;                 // waves per block (4)
+  int qt;                    // query tiles per block (1 or 2)
   int keys_ub;               // host upper bound of C + R (<= max_ctx): the split layout
   const void* q;             // [R][H][hd] activation planes
   size_t q_plane;
