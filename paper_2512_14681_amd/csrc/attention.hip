@@ -378,10 +378,16 @@ template <typename T, int HD>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const int nq = (a.H / a.G) * a.R;
   const int ntiles = (nq + 15) / 16;
-  if (a.qt == 2)
-    hipLaunchKernelGGL((k_attn<T, HD, 2>), dim3(a.G, (ntiles + 1) / 2, a.splits), dim3(256), 0, st, a);
-  else
+  // two query tiles per block: bf16 only (measured there; the fp32 kernel
+  // has no registers to spare)
+  bool two = false;
+  if constexpr (sizeof(T) == 2) two = a.qt == 2;
+  if (two) {
+    if constexpr (sizeof(T) == 2)
+      hipLaunchKernelGGL((k_attn<T, HD, 2>), dim3(a.G, (ntiles + 1) / 2, a.splits), dim3(256), 0, st, a);
+  } else {
     hipLaunchKernelGGL((k_attn<T, HD, 1>), dim3(a.G, ntiles, a.splits), dim3(256), 0, st, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   const dim3 grid(a.G, ntiles, HD / 32);

@@ -8,11 +8,11 @@
 // Point selection reads every point of every block once: HBM-bound, with
 // little data per block (a 16-token block's 17 points are 1088 bytes), so
 // the design goal is bytes in flight.  k_traj_select_multi gives each wave B
-// blocks: one load of their B lengths, then every point of all B blocks
-// loaded at once (when n <= 64 a load covers floor(64 / n) points:
-// 4 points of a 16-token block per coalesced 256-byte load), and the fixed
-// point y* taken from registers with a lane shuffle instead of a third,
-// dependent load; lane j then owns point j (so max_points <= 64 there).
+// blocks: one load of their B lengths, then every point of all B blocks and
+// their fixed points y* loaded at once through range-checked buffer loads
+// (when n <= 64 a load covers floor(64 / n) points: 4 points of a 16-token
+// block per coalesced 256-byte load); lane j then owns point j (so
+// max_points <= 64 there).
 // k_traj_select (one block per wave, any n and length) is the general path.
 // The unconverged count of a point is a popcount of the wave's mismatch
 // ballot; the choice is exact integer arithmetic, |u w - t_num n| minimal
@@ -121,10 +121,9 @@ __device__ __forceinline__ int wave_min_nonneg(int x) {
   return min(min(a, b), min(c, d));
 }
 
-// B blocks per wave, all of their points held in K registers per block
-// (K * floor(64 / n) >= max_points, n <= 64, max_points <= 64, w < 2^24,
-// n w < 2^25),
-// the fixed point in one more.
+// B blocks per wave, all of their points held in K registers per block and
+// the fixed point in one more (K * floor(64 / n) >= max_points, n <= 64,
+// max_points <= 64, w < 2^24, n w < 2^25).
 // Lane j takes point j's unconverged count u_j; a wave minimum over the key
 // (d_j << 6) | j, d_j = |u_j w - t n|, picks the point, the earliest on
 // ties.  The numerator t is clamped to [0, w] first: beyond that range d is
