@@ -50,12 +50,19 @@ class Decoder:
         i32 = torch.int32
         self.d_tokens = torch.zeros(R, dtype=i32, device=dev)
         self.d_next = torch.zeros(R, dtype=i32, device=dev)
-        # result (4 ints) and argmax (R ints) adjacent: one read per iteration
-        self.d_io = torch.zeros(4 + R, dtype=i32, device=dev)
+        # result (4 ints), argmax (R), per-segment counts and the committed
+        # path adjacent in one buffer: one device-to-host read per iteration
+        S = jf.JF_MAX_SEGMENTS
+        self.d_io = torch.zeros(4 + R + S + R, dtype=i32, device=dev)
         self.d_result = self.d_io[:4]
-        self.d_argmax = self.d_io[4:]
-        self.d_seg = torch.zeros(jf.JF_MAX_SEGMENTS, dtype=i32, device=dev)
-        self.d_path = torch.zeros(R, dtype=i32, device=dev)
+        self.d_argmax = self.d_io[4:4 + R]
+        self.d_seg = self.d_io[4 + R:4 + R + S]
+        self.d_path = self.d_io[4 + R + S:]
+        self._seg_at, self._path_at = 4 + R, 4 + R + S
+        # pinned staging of host-built drafts: the upload is ordered on the
+        # stream and needs no synchronisation (the buffer is rewritten only
+        # after the next result read, when that upload has long completed)
+        self.h_stage = torch.zeros(R, dtype=i32, pin_memory=True)
         self.d_pending = torch.zeros(1, dtype=i32, device=dev)
         self.trace = []
 
@@ -72,7 +79,9 @@ class Decoder:
         return int(self.d_pending.cpu()[0])
 
     def _put(self, buf, values):
-        buf[:len(values)].copy_(self.t.as_tensor(np.asarray(values, dtype=np.int32)), non_blocking=False)
+        k = len(values)
+        self.h_stage[:k].copy_(self.t.from_numpy(np.asarray(values, dtype=np.int32)))
+        buf[:k].copy_(self.h_stage[:k], non_blocking=True)
 
     # ---- Eq. 1 -----------------------------------------------------------------
     def generate_ar(self, prompt, max_new: int):
@@ -199,9 +208,9 @@ class Decoder:
                                  self.d_path)
             left = max_new - len(out)
             m.jf_commit_kv(self.d_path, self.d_result, left)
-            io = self.d_io[:4 + R].cpu().numpy()
-            seg_m = self.d_seg[:len(segs)].cpu().numpy()
-            path = self.d_path[:int(io[0])].cpu().numpy()
+            io = self.d_io.cpu().numpy()
+            seg_m = io[self._seg_at:self._seg_at + len(segs)]
+            path = io[self._path_at:self._path_at + int(io[0])]
             g = io[4:4 + R]
             a = min(int(io[0]), left)
             win = int(io[1])
