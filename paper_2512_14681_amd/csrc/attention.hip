@@ -4,9 +4,10 @@
 // marks (its ancestors and itself: a causal triangle for a linear draft, a
 // tree for multi-block / recycled candidates, Sec. 3.2 and App. A Alg. 1).
 //
-// Work split: block (kv head g, 16-query tile, key split).  The query rows
-// of a KV head are its n_heads/n_kv_heads query heads times R rows, 16 per
-// MFMA tile.  The key splits are laid out over the host's upper bound of
+// Work split: block (kv head g, 16-query tile, key split), or two query
+// tiles per block for bf16 when query tiles x keys is large (each key chunk
+// then serves both tiles).  The query rows of a KV head are its
+// n_heads/n_kv_heads query heads times R rows, 16 per MFMA tile.  The key splits are laid out over the host's upper bound of
 // C + R, so no address waits on the device's committed length (which only
 // masks), and the split's page-table entries are read once into LDS.  The
 // block's 4 waves take interleaved 32-key chunks with the next chunk's K/V
