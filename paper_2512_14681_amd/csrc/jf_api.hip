@@ -307,8 +307,10 @@ extern "C" jf_status jf_model_free(jf_model* m) {
 static jf_status prof_mark(jf_model* m, int cls, hipStream_t st) {
   if (m->prof_class != cls) return JF_OK;
   if (m->prof_used == m->prof_events.size()) {
+    // Timing only (read after a stream synchronisation): no system-scope
+    // fence, whose cache writeback would be counted in the kernel's time.
     hipEvent_t e;
-    HIP_TRY(hipEventCreate(&e));
+    HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
     m->prof_events.push_back(e);
   }
   HIP_TRY(hipEventRecord(m->prof_events[m->prof_used++], st));
