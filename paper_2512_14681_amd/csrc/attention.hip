@@ -403,7 +403,7 @@ static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
+static hipError_t launch_checked(int dtype, const AttnArgs& a, hipStream_t st) {
   if (a.R < 1 || a.R > 256 || a.splits < 1 || a.splits > kAttnMaxSplits || a.H % a.G || a.keys_ub < a.R ||
       a.keys_ub > a.max_ctx)
     return hipErrorInvalidValue;
@@ -420,6 +420,27 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
     case 128: return dtype == 1 ? launch_attn_t<bf16_t, 128>(a, st) : launch_attn_t<float, 128>(a, st);
     default: return hipErrorInvalidValue;
   }
+}
+
+// The two-tile form (bf16): its key splits are halved while the grid has
+// more than kAttnQt2Blocks blocks.  Measured on the attention workloads at
+// P = 8192 (32 splits from the one-tile plan): the wider combine of many
+// splits costs more than the extra blocks gain once the grid is that large.
+// Best were 16 splits at n = 16 (256 blocks, -9%) and n = 32 (448 blocks,
+// -29%), 8 at n = 64 (448 blocks, -41%); 256 or 512 as the bound each lost
+// one of them.
+constexpr int kAttnQt2Blocks = 448;
+
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
+  if (dtype == 1 && a.qt == 2) {
+    AttnArgs b = a;
+    const long pairs = ((long)((a.H / a.G) * a.R + 15) / 16 + 1) / 2;
+    const int min_s = (a.keys_ub + (kAttnMaxPages - 2) * kPage - 1) / ((kAttnMaxPages - 2) * kPage);
+    while (b.splits > 1 && (long)a.G * pairs * b.splits > kAttnQt2Blocks && (b.splits + 1) / 2 >= min_s)
+      b.splits = (b.splits + 1) / 2;
+    return launch_checked(dtype, b, st);
+  }
+  return launch_checked(dtype, a, st);
 }
 
 }  // namespace jf

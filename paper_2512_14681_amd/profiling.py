@@ -59,6 +59,27 @@ def stats(directory, top=25):
     return "\n".join(lines)
 
 
+def stats_by_grid(directory, pattern, top=40):
+    """Per (kernel, grid of workgroups) from the kernel trace: the launches of
+    one kernel at different shapes kept apart.  pattern: regex on the
+    short kernel name."""
+    pat = re.compile(pattern)
+    groups = {}
+    for r in _rows(directory, "kernel_trace.csv"):
+        name = short_name(r["kernel_name"])
+        if not pat.search(name):
+            continue
+        wg = tuple(int(r[f"workgroup_size_{a}"]) for a in "xyz")
+        grid = tuple(int(r[f"grid_size_{a}"]) // w for a, w in zip("xyz", wg))
+        dur = int(r["end_timestamp"]) - int(r["start_timestamp"])
+        groups.setdefault((name, grid), []).append(dur)
+    lines = ["| kernel | workgroups (x, y, z) | calls | avg us | min us |", "|---|---|---:|---:|---:|"]
+    for (name, grid), d in sorted(groups.items(), key=lambda kv: -sum(kv[1]))[:top]:
+        lines.append(f"| `{name[:60]}` | {grid[0]} x {grid[1]} x {grid[2]} | {len(d)} | "
+                     f"{sum(d) / len(d) / 1e3:.2f} | {min(d) / 1e3:.2f} |")
+    return "\n".join(lines)
+
+
 def _per_dispatch(directory, counter):
     """[(dispatch id, kernel name, value)] of one counter, in dispatch order."""
     out = []
@@ -107,6 +128,8 @@ def main(argv=None):
     s = sub.add_parser("stats")
     s.add_argument("dir")
     s.add_argument("--top", type=int, default=25)
+    s.add_argument("--by-grid", metavar="REGEX",
+                   help="kernels matching REGEX, one line per grid of workgroups (from the kernel trace)")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
@@ -116,7 +139,7 @@ def main(argv=None):
                    "(default: the GEMM sources)")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
-        print(stats(a.dir, a.top))
+        print(stats_by_grid(a.dir, a.by_grid, a.top) if a.by_grid else stats(a.dir, a.top))
     else:
         print(traffic(a.fetch, a.write, a.kernel, a.copy_bytes, a.sources))
 
