@@ -11,7 +11,15 @@
         whose name contains "copy" (a plain device copy of N bytes that the
         profiled program runs first, e.g. ``bench.py --copy-probe``).
 
-Both print Markdown; ``traffic`` ends with ``- key: value`` lines that
+    python -m paper_2512_14681_amd.profiling ceiling [--gib G] [--reps K]
+        HBM rates that plain library kernels reach on the device (GPU
+        required): a full read of a G GiB bf16 tensor (torch's sum, fp32
+        accumulation) and a device-to-device copy of it, each timed with
+        events over K calls after a warm-up.  G well above the 256 MB
+        Infinity Cache keeps both in HBM.  Also the library GEMM (torch's
+        matmul) on the 7B gate/up shape, 16 x 3584 x 37888 bf16.
+
+All print Markdown; ``traffic`` ends with ``- key: value`` lines that
 bench.py reads back (the SHA-256 of the GEMM sources pins the figure to the
 kernel it was measured on).
 """
@@ -122,6 +130,49 @@ def traffic(fetch_dir, write_dir, kernel_regex, copy_bytes, sources=None):
     ])
 
 
+def ceiling(gib=2.0, reps=20, peak_tbs=8.0):
+    import torch
+    n = int(gib * (1 << 30)) // 2
+    x = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    y = torch.empty_like(x)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+
+    rows = [("read (sum)", n * 2, timed(lambda: x.sum(dtype=torch.float32))),
+            ("copy (read + write)", n * 4, timed(lambda: y.copy_(x)))]
+    del x, y
+    # The library GEMM on the 7B gate/up shape (16 rows, K 3584, N 37888),
+    # rotating over four weight copies so that no call finds its weights in
+    # the Infinity Cache; bytes are the weights' alone, as for k_gemm.
+    K, N = 3584, 37888
+    ws = [torch.ones(N, K, dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+    xa = torch.ones(16, K, dtype=torch.bfloat16, device="cuda")
+    it = [0]
+
+    def gemm():
+        it[0] += 1
+        return torch.matmul(xa, ws[it[0] % 4].t())
+
+    rows.append(("library GEMM 16 x 3584 x 37888 (torch.matmul)", N * K * 2, timed(gemm)))
+    out = [f"{gib:g} GiB bf16 tensor, {reps} calls each after 3 warm-up calls, HIP events",
+           "", "| kernel | HBM bytes per call | us per call | TB/s | of " + f"{peak_tbs:g} TB/s |",
+           "|---|---:|---:|---:|---:|"]
+    for name, nbytes, t in rows:
+        out.append(f"| {name} | {nbytes:,} | {t * 1e6:.1f} | {nbytes / t / 1e12:.2f} | "
+                   f"{nbytes / t / 1e12 / peak_tbs:.3f} |")
+    return "\n".join(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -137,8 +188,13 @@ def main(argv=None):
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--sources", nargs="*", help="source files whose hashes the summary records "
                    "(default: the GEMM sources)")
+    c = sub.add_parser("ceiling")
+    c.add_argument("--gib", type=float, default=2.0)
+    c.add_argument("--reps", type=int, default=20)
     a = ap.parse_args(argv)
-    if a.cmd == "stats":
+    if a.cmd == "ceiling":
+        print(ceiling(a.gib, a.reps), flush=True)
+    elif a.cmd == "stats":
         print(stats_by_grid(a.dir, a.by_grid, a.top) if a.by_grid else stats(a.dir, a.top))
     else:
         print(traffic(a.fetch, a.write, a.kernel, a.copy_bytes, a.sources))
