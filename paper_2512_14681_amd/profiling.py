@@ -19,6 +19,12 @@
         Infinity Cache keeps both in HBM.  Also the library GEMM (torch's
         matmul) on the 7B gate/up shape, 16 x 3584 x 37888 bf16.
 
+    python -m paper_2512_14681_amd.profiling library-gemms [--rows R] [--reps K]
+        The projections of one 7B-shaped step as library GEMMs (torch's
+        matmul, bf16): per layer QKV, O, gate/up and down over 28 layers of
+        distinct weights, then the LM head; no attention, norms, epilogues
+        or argmax.  Timed with events over K passes after a warm-up.
+
 All print Markdown; ``traffic`` ends with ``- key: value`` lines that
 bench.py reads back (the SHA-256 of the GEMM sources pins the figure to the
 kernel it was measured on).
@@ -173,6 +179,42 @@ def ceiling(gib=2.0, reps=20, peak_tbs=8.0):
     return "\n".join(out)
 
 
+def library_gemms(rows=16, reps=10):
+    import torch
+    d, qkv, F, V, L = 3584, 4608, 18944, 152064, 28
+    shapes = [(qkv, d), (d, d), (2 * F, d), (d, F)]
+    layers = [[torch.ones(n, k, dtype=torch.bfloat16, device="cuda") for n, k in shapes] for _ in range(L)]
+    lm = torch.ones(V, d, dtype=torch.bfloat16, device="cuda")
+    x = torch.ones(rows, d, dtype=torch.bfloat16, device="cuda")
+    a = torch.ones(rows, F, dtype=torch.bfloat16, device="cuda")
+
+    def step():
+        for wq, wo, wgu, wd in layers:
+            torch.matmul(x, wq.t())
+            torch.matmul(x, wo.t())
+            torch.matmul(x, wgu.t())
+            torch.matmul(a, wd.t())
+        return torch.matmul(x, lm.t())
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        step()
+    e1.record()
+    e1.synchronize()
+    t = e0.elapsed_time(e1) / reps * 1e-3
+    nbytes = sum(n * k for n, k in shapes) * L * 2 + V * d * 2
+    return "\n".join([
+        f"7B-shaped step projections as library GEMMs, {rows} rows, {L} layers + LM head, "
+        f"{reps} passes after 2 warm-up passes, HIP events", "",
+        "| what | weight bytes per pass | ms per pass | TB/s | of 8 TB/s |", "|---|---:|---:|---:|---:|",
+        f"| {4 * L + 1} library GEMMs | {nbytes:,} | {t * 1e3:.3f} | {nbytes / t / 1e12:.2f} | "
+        f"{nbytes / t / 1e12 / 8.0:.3f} |"])
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -191,8 +233,13 @@ def main(argv=None):
     c = sub.add_parser("ceiling")
     c.add_argument("--gib", type=float, default=2.0)
     c.add_argument("--reps", type=int, default=20)
+    lg = sub.add_parser("library-gemms")
+    lg.add_argument("--rows", type=int, default=16)
+    lg.add_argument("--reps", type=int, default=10)
     a = ap.parse_args(argv)
-    if a.cmd == "ceiling":
+    if a.cmd == "library-gemms":
+        print(library_gemms(a.rows, a.reps), flush=True)
+    elif a.cmd == "ceiling":
         print(ceiling(a.gib, a.reps), flush=True)
     elif a.cmd == "stats":
         print(stats_by_grid(a.dir, a.by_grid, a.top) if a.by_grid else stats(a.dir, a.top))
