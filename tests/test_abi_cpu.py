@@ -118,3 +118,13 @@ def test_workspace_size_helpers(L):
     assert L.jf_lm_head_ws_bytes(64, 152064) >= 152064 // 16 * 64 * 8
     assert L.jf_packed_matrix_bytes(152064, 3584, 1) == 152064 * 3584 * 2
     assert L.jf_attention_ws_bytes(0, 128, 64) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    # No fallback: without the built library every call raises.
+    monkeypatch.setattr(jf, "_LIB", None)
+    monkeypatch.setattr(jf, "LIB_PATH", str(tmp_path / "libjf.so"))
+    with pytest.raises(RuntimeError, match="is missing"):
+        jf.lib()
+    with pytest.raises(RuntimeError, match="is missing"):
+        jf.query_sizes(tiny_cfg())
