@@ -97,12 +97,15 @@ __global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
   per = (per + 31) & ~31;
   const int k0 = split * per;
   const int k1 = min(a.keys_ub, k0 + per);
-  const int nch = k1 > k0 ? (k1 - k0 + 31) / 32 : 0;
   const int p0 = k0 / kPage;
   const int np = k1 > k0 ? (k1 - 1) / kPage - p0 + 1 : 0;
   for (int i = threadIdx.x; i < np; i += 64 * NW) s_pt[i] = a.page_table[p0 + i];
-  const int C = a.state ? a.state[0] : a.C_host;  // masks only
+  const int C = a.state ? a.state[0] : a.C_host;
   const int lim = min(k1, C + R);                 // keys at or past lim are not visible here
+  // Chunks up to lim only: when the host's bound runs ahead of the committed
+  // length, the masked keys past C + R are neither loaded nor computed, and a
+  // split that starts past them does no work.
+  const int nch = lim > k0 ? (lim - k0 + 31) / 32 : 0;
 
   const int ql = lane & 15, kg = lane >> 4;
   const T* kv = reinterpret_cast<const T*>(a.kv);

@@ -98,8 +98,9 @@ class Decoder:
     # ---- Eq. 3 / Eq. 4 / running window ------------------------------------------
     def generate_jacobi(self, prompt, n: int, max_new: int, mode: str = "window",
                         pad_seed: int = 2, logits=None):
-        """Returns (tokens, accept counts).  ``logits`` (optional list) gets the
-        fp32 logits of every iteration as numpy arrays."""
+        """Returns (tokens, accept counts).  ``logits`` (optional list) gets,
+        per iteration, the fp32 logits of the rows whose predictions were
+        committed: rows 0 .. a-1, row j predicting the token after draft[j]."""
         m, V = self.m, self.V
         p = self.prefill(prompt)
         C = len(prompt)
@@ -123,7 +124,7 @@ class Decoder:
             accepts.append(a)
             self.trace.append(dict(R=cur, a=a, g=g.copy()))
             if logits is not None:
-                logits.append(d_logits.cpu().numpy())
+                logits.append(d_logits[:a].cpu().numpy())
             p = int(g[a - 1])
             C += a
             if mode == "block":
@@ -169,8 +170,11 @@ class Decoder:
     # ---- App. A Alg. 1 ------------------------------------------------------------
     def generate_multiblock(self, prompt, n: int, K: int, r: float, max_new: int,
                             n_cand: int = 8, cand_len: int = 16, pool_cap: int = 64,
-                            pad_seed: int = 2):
-        """Multi-block decoding with rejection recycling; returns (tokens, trace)."""
+                            pad_seed: int = 2, logits=None):
+        """Multi-block decoding with rejection recycling; returns (tokens, trace).
+        ``logits`` (optional list) gets, per iteration, the fp32 logits of the
+        committed path's rows path[0 .. a-1], row path[j] predicting the
+        token committed after it."""
         m, V = self.m, self.V
         thr = math.ceil(r * n)
         p = self.prefill(prompt)
@@ -204,8 +208,11 @@ class Decoder:
                 toks += list(body)
             R = len(toks)
             self._put(self.d_tokens, toks)
+            d_logits = None
+            if logits is not None:
+                d_logits = self.t.empty((R, V), dtype=self.t.float32, device="cuda")
             m.jf_multiblock_step(self.d_tokens, R, segs, self.d_argmax, self.d_seg, self.d_result,
-                                 self.d_path)
+                                 self.d_path, d_logits)
             left = max_new - len(out)
             m.jf_commit_kv(self.d_path, self.d_result, left)
             io = self.d_io.cpu().numpy()
@@ -216,6 +223,8 @@ class Decoder:
             win = int(io[1])
             committed = [toks[i] for i in path[:a]]
             out += committed
+            if logits is not None:
+                logits.append(d_logits[self.t.as_tensor(path[:a].astype(np.int64), device="cuda")].cpu().numpy())
             trace.append(dict(R=R, segs=list(segs), m=[int(x) for x in seg_m], winner=win, a=a,
                               committed=committed))
             p_new = int(g[path[a - 1]])

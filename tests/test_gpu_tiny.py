@@ -194,3 +194,69 @@ def test_error_paths(env):
     m.jf_jacobi_step(d, 4, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
     res = dec.d_result.cpu().numpy()
     assert res[3] & jf.JF_FLAG_BAD_TOKEN
+
+
+@pytest.mark.parametrize("m_len", [1, 5, 8])
+def test_tree_commit_moves_winning_candidate(env, m_len):
+    """A recycled candidate that holds the oracle's greedy continuation wins
+    the step; the commit moves its rows' K/V from their in-step slots to
+    C + 1 .. C + m (source != destination), and the next step, run on the
+    moved cache, matches an oracle that committed the same rows (Sec. 3.2:
+    only the winning branch is committed; App. A Alg. 1 drops the rest)."""
+    import torch
+    from oracle import tree as otree
+    dec, jf_, model = env["dec"], env["jf"], env["model"]
+    V = SHAPE["vocab"]
+    n = 8
+    prompt = env["prompt"]
+    ar = ojac.generate_ar(oracle(env), prompt, n + 1)       # ar[0] = pending token
+    rng = np.random.default_rng(100 + m_len)
+    rand = lambda k: [int(t) for t in rng.integers(0, V, k)]
+    ra = [ar[0]] + rand(n - 1)
+    ra[1] = (ar[1] + 1) % V                                  # the Jacobi draft fails at once
+    cand_a = rand(n)
+    cand_b = ar[1:1 + m_len] + rand(n - m_len)
+    if m_len < n:
+        cand_b[m_len] = (ar[1 + m_len] + 1) % V              # stops after m_len rows
+    pseudo = rand(n)
+    tokens = ra + pseudo + cand_a + cand_b
+    segs = [(0, n, -1, jf_.JF_ROLE_RA, 1), (n, n, n - 1, jf_.JF_ROLE_PSEUDO, 0),
+            (2 * n, n, 0, jf_.JF_ROLE_CAND, 0), (3 * n, n, 0, jf_.JF_ROLE_CAND, 0)]
+    R = len(tokens)
+    dec.reset()
+    p = dec.prefill(prompt)
+    assert p == ar[0]
+    d_tok = torch.tensor(tokens, dtype=torch.int32, device="cuda")
+    d_log = torch.empty((R, V), dtype=torch.float32, device="cuda")
+    model.jf_multiblock_step(d_tok, R, segs, dec.d_argmax, dec.d_seg, dec.d_result, dec.d_path, d_log)
+    # oracle: the same step, its verification and winner
+    be = oracle(env)
+    be.prefill(prompt)
+    osegs = [otree.Segment(*s) for s in segs]
+    go, parent = be.step(tokens, osegs)
+    assert np.abs(d_log.cpu().numpy() - be.last[1]).max() < LOGIT_TOL
+    m = otree.verify(tokens, go, parent, osegs)
+    win, path = otree.winner_path(osegs, m, parent)
+    assert win == 3 and path == [0] + list(range(3 * n, 3 * n + m_len))
+    res = dec.d_result.cpu().numpy()
+    assert list(dec.d_seg.cpu().numpy()[:4]) == m
+    assert res[0] == len(path) and res[1] == win and res[2] == go[path[-1]]
+    assert list(dec.d_path.cpu().numpy()[:len(path)]) == path
+    # commit the winning path (its candidate rows move down to C + 1 ..)
+    model.jf_commit_kv(dec.d_path, dec.d_result)
+    be.commit(path)
+    assert dec.length() == be.length == len(prompt) + 1 + m_len
+    # next step on the moved cache
+    p2 = int(go[path[-1]])
+    draft = [p2] + [ojac.pad_id(9, be.length + i, V) for i in range(1, n)]
+    d_draft = torch.tensor(draft, dtype=torch.int32, device="cuda")
+    d_next = torch.zeros(n, dtype=torch.int32, device="cuda")
+    d_log2 = torch.empty((n, V), dtype=torch.float32, device="cuda")
+    model.jf_jacobi_step(d_draft, n, 1, 9, dec.d_argmax, dec.d_result, d_next, d_log2)
+    g2, _ = be.step(draft, ojac.linear_segments(n))
+    err = np.abs(d_log2.cpu().numpy() - be.last[1]).max()
+    assert err < LOGIT_TOL, err
+    gap = be.log[-1]["gap"]
+    assert ((dec.d_argmax[:n].cpu().numpy() == g2) | (gap < GAP_EXEMPT)).all()
+    # and the committed tokens are the greedy continuation
+    assert ar[:1 + m_len] == [tokens[r] for r in path]
