@@ -262,6 +262,27 @@ jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t dtype,
                             jf_step_result *d_result, float *d_logits,
                             void *d_ws, jf_stream stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation and outputs as jf_lm_head_accept, with no d_ws argument.  Its
+ * scratch (per-block argmax keys and one zeroed word) is a fixed device array
+ * inside libjf of JF_NOALLOC_SCRATCH_BYTES, one copy per GPU, held until the
+ * process ends; the call performs no hipMalloc / hipFree and enqueues only
+ * kernels.  R and V must satisfy jf_lm_head_ws_bytes(R, V) <=
+ * JF_NOALLOC_SCRATCH_BYTES (e.g. R <= 64 at V = 152064), else JF_E_CAPACITY
+ * and nothing is enqueued.  Every call on one GPU shares that GPU's array and
+ * leaves its contents behind; calls that overlap on one GPU (other streams,
+ * other threads) race and must be serialised by the caller.  The first call
+ * on each device looks up the array's device address (hipGetSymbolAddress);
+ * a failure there returns JF_E_HIP. */
+#define JF_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+jf_status jf_lm_head_accept_noalloc(int32_t R, int32_t d, int32_t V,
+                                    int32_t dtype, const void *d_x,
+                                    const void *d_w_packed,
+                                    const int32_t *d_draft, int32_t *d_argmax,
+                                    jf_step_result *d_result, float *d_logits,
+                                    jf_stream stream);
+
 /* ---- packed training sequences (forward only) -----------------------------
  * Sec. 3.1 (noise-aware causal attention) and App. C (sequence packing): a
  * training sequence interleaves, for each block i of a response, the noisy

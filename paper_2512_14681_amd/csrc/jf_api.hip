@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -755,6 +756,55 @@ extern "C" jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t 
                                  reinterpret_cast<int32_t*>(d_result), nullptr, st));
   }
   return JF_OK;
+}
+
+// ---- the LM-head component without caller workspace ----------------------------------
+// Its scratch (the per-block argmax keys and the zeroed committed-length word
+// the acceptance kernel takes) lives in this fixed device array: one copy per
+// GPU, held until the process ends.  Host code never passes the array's name
+// to a kernel (in host code it is a stand-in, not a device address); it uses
+// the device address read once per device with hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[JF_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of `scratch` on the current device (looked up once per device).
+static jf_status scratch_ptr(void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(JF_E_INVAL, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(JF_E_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return JF_OK;
+}
+
+extern "C" jf_status jf_lm_head_accept_noalloc(int32_t R, int32_t d, int32_t V, int32_t dtype, const void* d_x,
+                                               const void* d_w_packed, const int32_t* d_draft, int32_t* d_argmax,
+                                               jf_step_result* d_result, float* d_logits, jf_stream stream) {
+  if (!d_x || !d_w_packed || !d_argmax) return fail(JF_E_INVAL, "null pointer argument");
+  if (d_draft && !d_result) return fail(JF_E_INVAL, "acceptance needs d_result");
+  if (dtype != JF_F32 && dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", dtype);
+  if (R < 1 || R > 256) return fail(JF_E_CAPACITY, "R must be in [1, 256]");
+  if (d < 128 || d % 128 || V < 16 || V % 16) return fail(JF_E_SHAPE, "d multiple of 128, V multiple of 16");
+  const size_t need = jf_lm_head_ws_bytes(R, V);
+  if (need > JF_NOALLOC_SCRATCH_BYTES)
+    return fail(JF_E_CAPACITY, "R = %d, V = %d need %zu bytes of scratch; the fixed scratch holds %zu", R, V, need,
+                (size_t)JF_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  jf_status s = scratch_ptr(&ws);
+  if (s != JF_OK) return s;
+  return jf_lm_head_accept(R, d, V, dtype, d_x, d_w_packed, d_draft, d_argmax, d_result, d_logits, ws, stream);
 }
 
 // ---- trajectories ------------------------------------------------------------------------

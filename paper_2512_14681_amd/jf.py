@@ -95,6 +95,7 @@ _SIGS = {
     "jf_pack_matrix": (I32, [I32, I32, I32, P, P, P]),
     "jf_lm_head_ws_bytes": (SZ, [I32, I32]),
     "jf_lm_head_accept": (I32, [I32, I32, I32, I32, P, P, P, P, P, P, P, P]),
+    "jf_lm_head_accept_noalloc": (I32, [I32, I32, I32, I32, P, P, P, P, P, P, P]),
     "jf_packed_forward": (I32, [P, P, I32, I32, I32, P, P, P]),
     "jf_trajectory_record": (I32, [P, P, I32, I32, P, P]),
     "jf_trajectory_select": (I32, [P, P, I32, I32, I32, I32, P, P, P, P]),

@@ -90,6 +90,13 @@ def test_null_arguments_rejected_without_hip(L):
     assert L.jf_pack_matrix(20, 128, 1, P(1), P(1), None) == jf.JF_E_SHAPE
     assert L.jf_lm_head_accept(4, 100, 1024, 1, P(1), P(1), None, P(1), None, None, P(1), None) == jf.JF_E_SHAPE
     assert L.jf_lm_head_accept(4, 128, 1024, 1, P(1), P(1), P(1), P(1), None, None, P(1), None) == jf.JF_E_INVAL
+    # the allocation-free LM head: same checks, plus its fixed scratch capacity
+    assert L.jf_lm_head_accept_noalloc(4, 100, 1024, 1, P(1), P(1), None, P(1), None, None, None) == jf.JF_E_SHAPE
+    assert L.jf_lm_head_accept_noalloc(4, 128, 1024, 1, None, P(1), None, P(1), None, None, None) == jf.JF_E_INVAL
+    assert L.jf_lm_head_accept_noalloc(300, 128, 1024, 1, P(1), P(1), None, P(1), None, None, None) == jf.JF_E_CAPACITY
+    assert L.jf_lm_head_accept_noalloc(256, 3584, 152064, 1, P(1), P(1), None, P(1), None, None,
+                                       None) == jf.JF_E_CAPACITY
+    assert "scratch" in L.jf_last_error().decode()
     # packed forward and trajectories: argument checks happen before any HIP call
     assert L.jf_packed_forward(None, P(1), 2, 8, 0, P(1), None, None) == jf.JF_E_INVAL
     assert L.jf_trajectory_record(None, P(1), 16, 4, P(1), None) == jf.JF_E_INVAL
