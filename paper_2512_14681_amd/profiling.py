@@ -136,6 +136,85 @@ def traffic(fetch_dir, write_dir, kernel_regex, copy_bytes, sources=None):
     ])
 
 
+def algo_bytes_7b(n, ctx):
+    """Algorithmic HBM bytes per dispatch of each phase of a 7B-shaped step of
+    n rows at committed length ctx: weights once (bf16), activations in and
+    outputs out at bf16, the attention's prefix and in-step K/V."""
+    d, F, V, H, G, hd = 3584, 18944, 152064, 28, 4, 128
+    qkv_n = (H + 2 * G) * hd
+    return {
+        "qkv": qkv_n * d * 2 + n * d * 2 + n * qkv_n * 2,
+        "o": d * H * hd * 2 + n * H * hd * 2 + n * d * 2,
+        "gateup": 2 * F * d * 2 + n * d * 2 + n * F * 2,
+        "down": d * F * 2 + n * F * 2 + n * d * 2,
+        "attn": (ctx + n) * 2 * G * hd * 2 + 2 * n * H * hd * 2,
+        "lm_head": V * d * 2 + n * d * 2,
+    }
+
+
+def _step_phases(rows, layers):
+    """Labels the dispatches of the Jacobi steps in rows [(id, name, value)]
+    by phase, from the launch order of one forward: k_embed, then per layer
+    the QKV projection, attention (+ its split merge), the O projection, the
+    gate/up and the down projection, then the LM head and its tail.  A
+    forward is kept when it ends in an acceptance kernel (a step, not a
+    prefill chunk).  Returns {phase: [values]}."""
+    forwards, cur = [], None
+    for did, name, v in rows:
+        n = short_name(name)
+        if n.startswith("k_embed"):
+            cur = []
+            forwards.append(cur)
+        if cur is not None:
+            cur.append((n, v))
+    gemm_phase = ("qkv", "o", "gateup", "down")
+    out = {}
+    for f in forwards:
+        if not any(n.startswith("k_accept") for n, _ in f):
+            continue
+        gi = 0
+        for n, v in f:
+            if n.startswith("k_gemm"):
+                lab = "lm_head" if gi == 4 * layers else gemm_phase[gi % 4]
+                gi += 1
+            elif n.startswith("k_attn_combine"):
+                lab = "attn_combine"
+            elif n.startswith("k_attn"):
+                lab = "attn"
+            else:
+                lab = re.sub(r"<.*", "", n)
+            out.setdefault(lab, []).append(v)
+    return out
+
+
+def step_traffic(fetch_dir, write_dir, copy_bytes, layers=28, algo=None):
+    """HBM bytes per dispatch of every phase of the Jacobi steps in a
+    rocprofv3 --pmc run (FETCH_SIZE and WRITE_SIZE in separate runs), scaled
+    by a copy probe of copy_bytes (FETCH_SIZE counts half the bytes a copy
+    moves, WRITE_SIZE all of them, on this device)."""
+    per = {}
+    for label, directory, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = _per_dispatch(directory, counter)
+        copies = [v for _, k, v in rows if "copy" in k.lower()][:3]
+        if len(copies) < 3:
+            raise RuntimeError(f"{counter}: fewer than 3 copy dispatches in {directory}")
+        scale = copy_bytes / (sum(copies) / 3 * 1024)
+        for ph, vals in _step_phases(rows, layers).items():
+            per.setdefault(ph, {})[label] = (sum(vals) / len(vals) * 1024 * scale, len(vals), scale)
+    lines = ["| phase | dispatches | FETCH bytes | WRITE bytes | HBM bytes per dispatch | algorithmic bytes | ratio |",
+             "|---|---:|---:|---:|---:|---:|---:|"]
+    order = ["qkv", "attn", "attn_combine", "o", "gateup", "down", "lm_head"]
+    for ph in order + sorted(k for k in per if k not in order):
+        if ph not in per or "fetch" not in per[ph] or "write" not in per[ph]:
+            continue
+        fb, n, _ = per[ph]["fetch"]
+        wb, _, _ = per[ph]["write"]
+        a = (algo or {}).get(ph)
+        lines.append(f"| {ph} | {n} | {fb:,.0f} | {wb:,.0f} | {fb + wb:,.0f} | "
+                     f"{f'{a:,}' if a else '—'} | {f'{(fb + wb) / a:.3f}' if a else '—'} |")
+    return "\n".join(lines)
+
+
 def ceiling(gib=2.0, reps=20, peak_tbs=8.0):
     import torch
     n = int(gib * (1 << 30)) // 2
@@ -230,6 +309,13 @@ def main(argv=None):
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--sources", nargs="*", help="source files whose hashes the summary records "
                    "(default: the GEMM sources)")
+    stt = sub.add_parser("step-traffic", help="HBM bytes of every phase of the Jacobi steps in a --pmc run")
+    stt.add_argument("--fetch", required=True)
+    stt.add_argument("--write", required=True)
+    stt.add_argument("--copy-bytes", type=int, required=True)
+    stt.add_argument("--layers", type=int, default=28)
+    stt.add_argument("--n", type=int, default=16, help="rows of the steps (for the algorithmic bytes)")
+    stt.add_argument("--ctx", type=int, default=1024, help="committed length (for the attention bytes)")
     c = sub.add_parser("ceiling")
     c.add_argument("--gib", type=float, default=2.0)
     c.add_argument("--reps", type=int, default=20)
@@ -241,6 +327,8 @@ def main(argv=None):
         print(library_gemms(a.rows, a.reps), flush=True)
     elif a.cmd == "ceiling":
         print(ceiling(a.gib, a.reps), flush=True)
+    elif a.cmd == "step-traffic":
+        print(step_traffic(a.fetch, a.write, a.copy_bytes, a.layers, algo_bytes_7b(a.n, a.ctx)))
     elif a.cmd == "stats":
         print(stats_by_grid(a.dir, a.by_grid, a.top) if a.by_grid else stats(a.dir, a.top))
     else:
