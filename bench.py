@@ -571,13 +571,15 @@ def main():
     kern = {}
     classes = () if args.no_kernel_profile else (
         (jf.JF_KERNEL_GATEUP, "gateup"), (jf.JF_KERNEL_DOWN, "down"), (jf.JF_KERNEL_QKV, "qkv"),
-        (jf.JF_KERNEL_O, "o"), (jf.JF_KERNEL_ATTN, "attn"), (jf.JF_KERNEL_LMHEAD, "lmhead"))
+        (jf.JF_KERNEL_O, "o"), (jf.JF_KERNEL_ATTN, "attn"), (jf.JF_KERNEL_ATTN_BLOCK, "attn_block"),
+        (jf.JF_KERNEL_LMHEAD, "lmhead"))
     for cls, name in classes:
         model.jf_profile_begin(cls)
         for i in range(K // 2):
             step(W + K + (i % K))
         t, cnt = model.jf_profile_end()
-        kern[name] = dict(avg_us=t / cnt * 1e3, launches=cnt)
+        if cnt:          # a class the step does not launch (fused away) records nothing
+            kern[name] = dict(avg_us=t / cnt * 1e3, launches=cnt)
         model.jf_kv_truncate(C0 + int(acc.sum()))
     if not kern:
         log("per-kernel pass skipped; no roofline object")

@@ -57,7 +57,7 @@ struct Layout {
   size_t page_bytes, kv_layer_bytes, kv_bytes;
   // workspace (bytes)
   size_t w_state, w_h, w_xn, w_q, w_attn, w_act, w_opart, w_ml, w_lm, w_g, w_parent, w_pos,
-      w_vis, w_cos, w_sin, w_pt, w_rowmap, w_result, w_kpart, w_kcount, w_ss, ws_bytes;
+      w_vis, w_cos, w_sin, w_pt, w_rowmap, w_result, w_kpart, w_kcount, w_ss, w_sync, ws_bytes;
 };
 
 jf_status check_config(const jf_config* c) {
@@ -131,6 +131,8 @@ Layout make_layout(const jf_config& c) {
   L.w_kcount = off; off = align_up(off + kGemmCounters * 4);
   // RMSNorm sums of squares: two fixed-point accumulators of 3 word planes
   L.w_ss = off; off = align_up(off + 2 * 3 * Rp * 8);
+  // flags and counters of the fused attention launch
+  L.w_sync = off; off = align_up(off + kAttnBlockSyncWords * 4);
   L.ws_bytes = off;
   return L;
 }
@@ -146,6 +148,10 @@ struct jf_model {
   int C_ub;          // host upper bound of the committed length
   int last_rows;     // rows of the last step (0: no step to commit)
   int last_tree;     // last step was a multi-block step
+  int fused_attention = 0;            // JF_OPT_FUSED_ATTENTION (measured slower; off by default)
+  int n_cus = 0;                      // compute units of the model's device
+  int attn_block_occ = 0;             // fused attention workgroups per compute unit
+  uint32_t epoch = 0;                 // launches of the fused attention (never 0 once used)
   int prof_class = 0;                 // kernel class being timed (0: none)
   std::vector<hipEvent_t> prof_events;  // pairs (start, end), reused
   size_t prof_used = 0;
@@ -255,6 +261,13 @@ extern "C" jf_status jf_model_load(const jf_config* cfg, const void* const* d_we
   LOAD_TRY(hipMemsetAsync(d_kv, 0, L.kv_bytes, st));
   LOAD_TRY(hipMemsetAsync(m->ws + L.w_state, 0, 64, st));
   LOAD_TRY(hipMemsetAsync(m->ws + L.w_kcount, 0, kGemmCounters * 4, st));
+  LOAD_TRY(hipMemsetAsync(m->ws + L.w_sync, 0, kAttnBlockSyncWords * 4, st));
+  {
+    int dev = 0;
+    LOAD_TRY(hipGetDevice(&dev));
+    LOAD_TRY(hipDeviceGetAttribute(&m->n_cus, hipDeviceAttributeMultiprocessorCount, dev));
+    m->attn_block_occ = attn_block_occupancy(c.head_dim);
+  }
   LOAD_TRY(hipMemcpyAsync(m->ws + L.w_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, st));
   LOAD_TRY(hipMemcpyAsync(m->ws + L.w_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, st));
   LOAD_TRY(hipMemcpyAsync(m->ws + L.w_pt, pt.data(), pt.size() * 4, hipMemcpyHostToDevice, st));
@@ -323,9 +336,17 @@ static jf_status prof_mark(jf_model* m, int cls, hipStream_t st) {
     if (ps_ != JF_OK) return ps_;                   \
   } while (0)
 
+extern "C" jf_status jf_model_set_option(jf_model* m, int32_t option, int32_t value) {
+  if (!m) return fail(JF_E_INVAL, "model is null");
+  if (option != JF_OPT_FUSED_ATTENTION) return fail(JF_E_INVAL, "unknown option %d", option);
+  if (value != 0 && value != 1) return fail(JF_E_INVAL, "option %d takes 0 or 1, got %d", option, value);
+  m->fused_attention = value;
+  return JF_OK;
+}
+
 extern "C" jf_status jf_profile_begin(jf_model* m, int32_t kernel_class) {
   if (!m) return fail(JF_E_INVAL, "model is null");
-  if (kernel_class < JF_KERNEL_QKV || kernel_class > JF_KERNEL_STEP)
+  if (kernel_class < JF_KERNEL_QKV || kernel_class > JF_KERNEL_ATTN_BLOCK)
     return fail(JF_E_INVAL, "unknown kernel class %d", kernel_class);
   m->prof_class = kernel_class;
   m->prof_used = 0;
@@ -394,10 +415,43 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
   HIP_TRY(launch_embed(dt, d_tokens, R, m->packed + L.p_embed, (const float*)(m->layer(0) + L.l_an), d,
                        c.vocab, h, xn, pl_d, ss_a, ss_f, ss_stride, m->flags(), st));
   const int keys_ub = std::min(m->C_ub + R, c.max_ctx);
+  // The attention half of every layer as one persistent launch (layer.hip)
+  // when the step qualifies; its plan is the same for all layers.
+  SideArgs sa{};
+  bool fused = m->fused_attention && dt == JF_BF16 && hd == 128 && R <= kAttnBlockMaxRows &&
+               m->attn_block_occ >= 1 && m->n_cus >= 1 && Hhd <= 4096 && d <= 4096 &&
+               m->L.qkv_rows / 16 <= kAttnBlockMaxTiles;
+  if (fused) {
+    sa.R = R; sa.d = d; sa.H = H; sa.G = G; sa.hd = hd; sa.max_ctx = c.max_ctx;
+    sa.qkv_tiles = m->L.qkv_rows / 16; sa.o_tiles = d / 16;
+    sa.kc_qkv = d / 128; sa.kc_o = Hhd / 128;
+    sa.p_qkv = pack_group(m->L.qkv_rows); sa.p_o = pack_group(d);
+    sa.keys_ub = keys_ub;
+    attn_block_plan(sa);
+    fused = sa.G * sa.qtiles <= kAttnBlockMaxGT && sa.splits <= kAttnMaxSplits && sa.kc_o <= 32;
+  }
   for (int l = 0; l < c.n_layers; ++l) {
     char* lp = m->layer(l);
+    if (fused) {
+      sa.x = xn; sa.x_plane = pl_d; sa.w_qkv = lp + L.l_qkv;
+      sa.ss_in = ss_a; sa.ss_stride = ss_stride; sa.norm_inv_d = 1.0 / d; sa.norm_eps = c.rms_eps;
+      sa.q = m->ws + L.w_q; sa.q_plane = pl_h; sa.kv = m->kv_layer(l);
+      sa.page_table = m->at<int32_t>(L.w_pt); sa.pos = pos; sa.state = state;
+      sa.rope_cos = m->at<float>(L.w_cos); sa.rope_sin = m->at<float>(L.w_sin); sa.flags = m->flags();
+      sa.vis = m->at<uint64_t>(L.w_vis);
+      sa.o_part = m->at<float>(L.w_opart); sa.ml_part = m->at<float>(L.w_ml);
+      sa.attn = m->ws + L.w_attn; sa.attn_plane = pl_h;
+      sa.w_o = lp + L.l_o; sa.h = h; sa.gain_next = (const float*)(lp + L.l_fn);
+      sa.xg = xn; sa.xg_plane = pl_d; sa.ss_out = ss_f; sa.ss_clear = ss_a;
+      sa.sync = m->at<uint32_t>(L.w_sync);
+      if (++m->epoch == 0) ++m->epoch;
+      sa.epoch = m->epoch;
+      PROF(JF_KERNEL_ATTN_BLOCK);
+      HIP_TRY(launch_attn_block(sa, m->n_cus, st));
+      PROF(JF_KERNEL_ATTN_BLOCK);
+    }
     // a3: attention RMSNorm (folded) + QKV + RoPE + K/V into the cache slots C + r
-    {
+    if (!fused) {
       GemmShape gs{R, m->L.qkv_rows, d, 1, 1, 1};
       gemm_plan(gs, EPI_QKV);
       Epi ep = m->epi();
@@ -412,7 +466,7 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
       PROF(JF_KERNEL_QKV);
     }
     // a4: attention
-    {
+    if (!fused) {
       AttnArgs a{};
       a.H = H; a.G = G; a.hd = hd; a.R = R; a.max_ctx = c.max_ctx; a.keys_ub = keys_ub;
       attn_plan(a);
@@ -425,7 +479,7 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
       PROF(JF_KERNEL_ATTN);
     }
     // a5: O projection + residual, writing the FFN RMSNorm's input
-    {
+    if (!fused) {
       GemmShape gs{R, d, Hhd, 1, 1, 1};
       gemm_plan(gs, EPI_RESID);
       Epi ep = m->epi();

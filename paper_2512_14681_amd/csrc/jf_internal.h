@@ -146,6 +146,56 @@ void attn_plan(AttnArgs& a);
 constexpr int kAttnChunksPerWave = 2;  // 32-key chunks per wave
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t stream);
 
+// The attention half of a layer (QKV + attention + O) in one persistent
+// launch, for bf16 steps of at most kAttnBlockMaxRows rows (layer.hip).
+constexpr int kAttnBlockMaxRows = 16;
+constexpr int kAttnBlockMaxGT = 256;      // kv heads x query tiles
+constexpr int kAttnBlockMaxTiles = 1024;  // 16-column tiles of the QKV projection
+constexpr int JF_FLAG_SYNC_BIT = 4;       // JF_FLAG_SYNC of jf.h
+// uint32 words of the launch's flags and counters (caller-owned, zeroed once)
+constexpr size_t kAttnBlockSyncWords = kAttnBlockMaxTiles + 3 * kAttnBlockMaxGT;
+struct SideArgs {
+  int R, d, H, G, hd, max_ctx;
+  int qkv_tiles, o_tiles;       // 16-column tiles of the two projections
+  int kc_qkv, kc_o;             // 128-wide K-blocks of the two projections
+  int p_qkv, p_o;               // pack groups of the two packed matrices
+  const void* x;                // attention norm's input (h * gain), GEMM-input layout
+  size_t x_plane;
+  const void* w_qkv;
+  const uint64_t* ss_in;        // the rows' fixed-point sums of squares of h
+  int ss_stride;
+  double norm_inv_d, norm_eps;
+  void* q;                      // [R][H][hd] activation planes
+  size_t q_plane;
+  void* kv;                     // this layer's pages
+  const int32_t* page_table;
+  const int32_t* pos;
+  const int32_t* state;         // state[0] = committed length C
+  const float* rope_cos;
+  const float* rope_sin;
+  int32_t* flags;               // step flags (JF_FLAG_*)
+  const uint64_t* vis;          // [R][4] in-step visibility, or null (causal)
+  int keys_ub;                  // host bound of C + R: the key-split layout
+  int qtiles, splits, split_keys;
+  float* o_part;                // [splits][R * H][hd]
+  float* ml_part;               // [splits][R * H][2]
+  void* attn;                   // merged attention output, GEMM-input layout [Rp][H * hd]
+  size_t attn_plane;
+  const void* w_o;
+  float* h;                     // residual stream [R][d]
+  const float* gain_next;       // next RMSNorm's gain
+  void* xg;                     // its input planes (GEMM-input layout [Rp][d])
+  size_t xg_plane;
+  uint64_t* ss_out;             // row sums of squares of the new h
+  uint64_t* ss_clear;           // zeroed after every QKV tile has read ss_in
+  uint32_t* sync;               // kAttnBlockSyncWords words
+  uint32_t epoch;               // this launch's number (never 0)
+};
+size_t attn_block_lds_bytes(int hd);
+int attn_block_occupancy(int hd);   // workgroups per compute unit (0: cannot run)
+void attn_block_plan(SideArgs& a);  // qtiles, splits, split_keys from R, H, G, keys_ub
+hipError_t launch_attn_block(const SideArgs& a, int n_blocks, hipStream_t stream);
+
 hipError_t launch_argmax_reduce(const uint64_t* part, int nblocks, int stride, int R,
                                 int32_t* g, hipStream_t stream);
 hipError_t launch_accept_linear(const int32_t* draft, const int32_t* g, int n, int mode,

@@ -20,10 +20,11 @@ JF_OK, JF_E_INVAL, JF_E_SHAPE, JF_E_CAPACITY, JF_E_DTYPE, JF_E_HIP, JF_E_STATE =
 JF_F32, JF_BF16 = 0, 1
 JF_ROLE_RA, JF_ROLE_CAND, JF_ROLE_PSEUDO = 0, 1, 2
 JF_MAX_SEGMENTS = 16
-JF_FLAG_BAD_TOKEN, JF_FLAG_CAPACITY = 1, 2
+JF_FLAG_BAD_TOKEN, JF_FLAG_CAPACITY, JF_FLAG_SYNC = 1, 2, 4
+JF_OPT_FUSED_ATTENTION = 1
 JF_MASK_NOISY_CONTEXT, JF_MASK_CLEAN_CONTEXT = 0, 1
 (JF_KERNEL_QKV, JF_KERNEL_ATTN, JF_KERNEL_O, JF_KERNEL_GATEUP, JF_KERNEL_DOWN, JF_KERNEL_LMHEAD,
- JF_KERNEL_STEP) = range(1, 8)
+ JF_KERNEL_STEP, JF_KERNEL_ATTN_BLOCK) = range(1, 9)
 STATUS_NAMES = {0: "JF_OK", -1: "JF_E_INVAL", -2: "JF_E_SHAPE", -3: "JF_E_CAPACITY",
                 -4: "JF_E_DTYPE", -5: "JF_E_HIP", -6: "JF_E_STATE"}
 
@@ -87,6 +88,7 @@ _SIGS = {
     "jf_kv_length": (I32, [P, ctypes.POINTER(I32), P]),
     "jf_kv_truncate": (I32, [P, I32, P]),
     "jf_kv_set_page_table": (I32, [P, ctypes.POINTER(I32), I32, P]),
+    "jf_model_set_option": (I32, [P, I32, I32]),
     "jf_profile_begin": (I32, [P, I32]),
     "jf_profile_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]),
     "jf_attention_ws_bytes": (SZ, [I32, I32, I32]),
@@ -231,6 +233,9 @@ class Model:
 
     def jf_kv_truncate(self, n):
         check(lib().jf_kv_truncate(self.h, int(n), _stream(self.stream)))
+
+    def jf_model_set_option(self, option, value):
+        check(lib().jf_model_set_option(self.h, int(option), int(value)))
 
     def jf_profile_begin(self, kernel_class):
         check(lib().jf_profile_begin(self.h, int(kernel_class)))

@@ -147,6 +147,33 @@ def test_7b_step_window_logits(env, prompt1024, n):
         assert res[0] >= t + 1
 
 
+def test_7b_fused_attention_equals_four_launches(env, prompt1024):
+    """The benchmark's step (n = 16) with QKV + attention + O of each layer
+    in one persistent launch and with the four separate launches: the same
+    logits up to fp32 summation order, no sync error."""
+    import torch
+    from paper_2512_14681_amd import jf
+    dec, model = env["dec"], env["model"]
+    n = 16
+    outs = []
+    for fused in (1, 0):
+        model.jf_model_set_option(jf.JF_OPT_FUSED_ATTENTION, fused)
+        dec.reset()
+        p = dec.prefill(prompt1024)
+        draft = [p] + [ojac.pad_id(2, 1024 + i, V) for i in range(1, n)]
+        d_draft = torch.tensor(draft, dtype=torch.int32, device="cuda")
+        d_next = torch.zeros(n, dtype=torch.int32, device="cuda")
+        d_log = torch.empty((n, V), dtype=torch.float32, device="cuda")
+        model.jf_jacobi_step(d_draft, n, 1, 2, dec.d_argmax, dec.d_result, d_next, d_log)
+        res = dec.d_result.cpu().numpy()
+        assert res[3] == 0, res
+        outs.append(d_log.cpu().numpy())
+    model.jf_model_set_option(jf.JF_OPT_FUSED_ATTENTION, 0)
+    err = np.abs(outs[0] - outs[1]).max()
+    say(f"fused vs four launches: max |logit difference| = {err:.2e}")
+    assert err < LOGIT_TOL
+
+
 @pytest.mark.parametrize("n", [16, 32])
 def test_7b_window_decode_is_greedy(env, prompt1024, n):
     """256 new tokens as benchmarked.  Every decoded position is checked

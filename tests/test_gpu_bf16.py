@@ -105,3 +105,55 @@ def test_repeat_is_bitwise_deterministic(env):
         env["model"].jf_jacobi_step(d, 16, 1, 0, dec.d_argmax, dec.d_result, dec.d_next, d_log)
         outs.append(d_log.cpu().numpy())
     assert np.array_equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("n", [1, 5, 16])
+def test_fused_attention_launch_equals_four_launches(env, n):
+    """Steps of at most 16 rows run QKV + attention + O of a layer as one
+    persistent launch (JF_OPT_FUSED_ATTENTION); the same step with the four
+    separate launches gives the same logits (to fp32 summation order: both
+    agree with the oracle within the bar), the same argmax away from
+    near-ties, and no sync error."""
+    import torch
+    from paper_2512_14681_amd import jf
+    dec, model = env["dec"], env["model"]
+    outs = []
+    for fused in (1, 0):
+        model.jf_model_set_option(jf.JF_OPT_FUSED_ATTENTION, fused)
+        dec.reset()
+        p = dec.prefill(env["prompt"])
+        draft = [p] + [ojac.pad_id(3, 80 + i, SHAPE["vocab"]) for i in range(1, n)]
+        d_draft = torch.tensor(draft, dtype=torch.int32, device="cuda")
+        d_next = torch.zeros(n, dtype=torch.int32, device="cuda")
+        d_log = torch.empty((n, SHAPE["vocab"]), dtype=torch.float32, device="cuda")
+        model.jf_jacobi_step(d_draft, n, 1, 3, dec.d_argmax, dec.d_result, d_next, d_log)
+        res = dec.d_result.cpu().numpy()
+        assert res[3] == 0, res
+        outs.append((d_log.cpu().numpy(), dec.d_argmax[:n].cpu().numpy(), res.copy(), draft))
+    model.jf_model_set_option(jf.JF_OPT_FUSED_ATTENTION, 0)
+    (z1, g1, r1, draft), (z0, g0, r0, _) = outs
+    assert np.abs(z1 - z0).max() < 1e-3
+    zo = teacher_forced(env, list(env["prompt"]) + draft)[80:80 + n]
+    assert np.abs(z1 - zo).max() < LOGIT_TOL
+    ok = (g1 == zo.argmax(1)) | (gaps(zo) < GAP_EXEMPT)
+    assert ok.all()
+    assert ((g1 == g0) | (gaps(zo) < GAP_EXEMPT)).all()
+
+
+def test_fused_attention_repeat_is_bitwise_deterministic(env):
+    """The fused launch merges waves, key splits and K-blocks in a fixed
+    order: two identical steps agree bit for bit."""
+    import torch
+    from paper_2512_14681_amd import jf
+    dec = env["dec"]
+    env["model"].jf_model_set_option(jf.JF_OPT_FUSED_ATTENTION, 1)
+    outs = []
+    for _ in range(2):
+        dec.reset()
+        p = dec.prefill(env["prompt"])
+        d = torch.tensor([p] + list(range(1, 12)), dtype=torch.int32, device="cuda")
+        d_log = torch.empty((12, SHAPE["vocab"]), dtype=torch.float32, device="cuda")
+        env["model"].jf_jacobi_step(d, 12, 1, 0, dec.d_argmax, dec.d_result, dec.d_next, d_log)
+        outs.append(d_log.cpu().numpy())
+    env["model"].jf_model_set_option(jf.JF_OPT_FUSED_ATTENTION, 0)
+    assert np.array_equal(outs[0], outs[1])
