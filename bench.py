@@ -484,7 +484,7 @@ def main():
                     help="skip the per-kernel event pass (for hardware-counter runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 256 MiB device-to-device 3 times (counter calibration)")
-    ap.add_argument("--only", choices=["trajectory_select", "attention"],
+    ap.add_argument("--only", choices=["trajectory_select", "attention", "lm_head"],
                     help="run one component workload alone and print its JSON object")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the other workloads (configs 1, 2, 3, 4 at n=32 and 64, 5)")
@@ -516,6 +516,9 @@ def main():
         return
     if args.only == "attention":
         print(json.dumps(bench_attention()), flush=True)
+        return
+    if args.only == "lm_head":
+        print(json.dumps(bench_lm_head()), flush=True)
         return
     shape = jf_inputs.MODEL_SHAPES["7b"]
     n, K, W = args.n, args.steps, args.warmup

@@ -11,7 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libjf.so")
-SOURCES = ["jf_api.hip", "gemm.hip", "attention.hip", "layer.hip", "step.hip", "trajectory.hip"]
+SOURCES = ["jf_api.hip", "gemm.hip", "gemm_mr.hip", "attention.hip", "layer.hip", "step.hip", "trajectory.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "--offload-arch=gfx950", "-fPIC", "-std=c++17", "-Wall",

@@ -370,6 +370,41 @@ extern "C" jf_status jf_profile_end(jf_model* m, double* total_ms, int32_t* laun
   return JF_OK;
 }
 
+// ---- projections ----------------------------------------------------------------------
+// Compute units of the current device (looked up once).
+static int device_cus() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) ==
+                                                 hipSuccess)
+      cus = n;
+  }
+  return cus > 0 ? cus : 256;
+}
+
+// One projection Y[R][N] = X[R][K] W^T with epilogue ep: the many-row kernel
+// (gemm_mr.hip) for bf16 with more than 32 rows, else the weight-streaming
+// kernel.  *part_blocks (if not null) gets the number of per-row argmax key
+// slots the launch writes (EPI_ARGMAX).  split_k = false keeps K in one
+// workgroup (callers without split-K scratch).
+static hipError_t run_gemm(int dtype, int R, int N, int K, const void* X, size_t xplane, const void* W, const Epi& ep,
+                           hipStream_t st, int* part_blocks = nullptr, bool split_k = true) {
+  if (dtype == JF_BF16 && R > 32 && ep.row0 == 0) {
+    MrPlan mp{};
+    if (gemm_mr_plan(mp, R, N, K, ep.kind, device_cus())) {
+      if (!split_k) mp.S = 1;
+      if (part_blocks) *part_blocks = mp.n_cg * mp.passes;
+      return launch_gemm_mr(X, xplane, W, mp, ep, st);
+    }
+  }
+  GemmShape gs{R, N, K, 1, 1, 1};
+  gemm_plan(gs, ep.kind);
+  if (!split_k) gs.S = 1;
+  if (part_blocks) *part_blocks = (int)gemm_blocks(gs);
+  return launch_gemm(dtype, X, xplane, W, gs, ep, st);
+}
+
 // ---- forward pass of one step ---------------------------------------------------------
 // Runs rows through all layers; the K/V of row r land in cache slot C + r.
 // lm: 0 = no LM head, 1 = all rows, 2 = last row only.  g receives the argmax.
@@ -452,8 +487,6 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
     }
     // a3: attention RMSNorm (folded) + QKV + RoPE + K/V into the cache slots C + r
     if (!fused) {
-      GemmShape gs{R, m->L.qkv_rows, d, 1, 1, 1};
-      gemm_plan(gs, EPI_QKV);
       Epi ep = m->epi();
       ep.kind = EPI_QKV; ep.R = R;
       norm_in(ep, ss_a);
@@ -462,7 +495,7 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
       ep.pos = pos; ep.state = state; ep.rope_cos = m->at<float>(L.w_cos); ep.rope_sin = m->at<float>(L.w_sin);
       ep.H = H; ep.G = G; ep.hd = hd; ep.max_ctx = c.max_ctx; ep.flags = m->flags();
       PROF(JF_KERNEL_QKV);
-      HIP_TRY(launch_gemm(dt, xn, pl_d, lp + L.l_qkv, gs, ep, st));
+      HIP_TRY(run_gemm(dt, R, m->L.qkv_rows, d, xn, pl_d, lp + L.l_qkv, ep, st));
       PROF(JF_KERNEL_QKV);
     }
     // a4: attention
@@ -480,31 +513,25 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
     }
     // a5: O projection + residual, writing the FFN RMSNorm's input
     if (!fused) {
-      GemmShape gs{R, d, Hhd, 1, 1, 1};
-      gemm_plan(gs, EPI_RESID);
       Epi ep = m->epi();
       ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
       norm_out(ep, (const float*)(lp + L.l_fn), ss_f, ss_a);
       PROF(JF_KERNEL_O);
-      HIP_TRY(launch_gemm(dt, m->ws + L.w_attn, pl_h, lp + L.l_o, gs, ep, st));
+      HIP_TRY(run_gemm(dt, R, d, Hhd, m->ws + L.w_attn, pl_h, lp + L.l_o, ep, st));
       PROF(JF_KERNEL_O);
     }
     // a6: FFN RMSNorm (folded), gate/up + SwiGLU, down + residual
     {
-      GemmShape gs{R, 2 * F, d, 2, 1, 1};
-      gemm_plan(gs, EPI_SWIGLU);
       Epi ep = m->epi();
       ep.kind = EPI_SWIGLU; ep.R = R; ep.act = m->ws + L.w_act; ep.act_k = F; ep.act_plane = pl_f;
       norm_in(ep, ss_f);
       PROF(JF_KERNEL_GATEUP);
-      HIP_TRY(launch_gemm(dt, xn, pl_d, lp + L.l_gu, gs, ep, st));
+      HIP_TRY(run_gemm(dt, R, 2 * F, d, xn, pl_d, lp + L.l_gu, ep, st));
       PROF(JF_KERNEL_GATEUP);
     }
     // down projection + residual, writing the next RMSNorm's input (the next
     // layer's attention norm, or the final norm before the LM head)
     {
-      GemmShape gs{R, d, F, 1, 1, 1};
-      gemm_plan(gs, EPI_RESID);
       Epi ep = m->epi();
       ep.kind = EPI_RESID; ep.R = R; ep.f32 = h; ep.ldf = d;
       if (l + 1 < c.n_layers)
@@ -512,7 +539,7 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
       else if (lm != 0)
         norm_out(ep, (const float*)(m->packed + L.p_final), ss_a, ss_f);
       PROF(JF_KERNEL_DOWN);
-      HIP_TRY(launch_gemm(dt, m->ws + L.w_act, pl_f, lp + L.l_down, gs, ep, st));
+      HIP_TRY(run_gemm(dt, R, d, F, m->ws + L.w_act, pl_f, lp + L.l_down, ep, st));
       PROF(JF_KERNEL_DOWN);
     }
   }
@@ -520,17 +547,16 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
   // a7: final RMSNorm (folded) + LM head with fused argmax (logits optional);
   // lm == 2 reads only the last row
   const int Rl = lm == 2 ? 1 : R;
-  GemmShape gs{Rl, c.vocab, d, 1, 1, 1};
-  gemm_plan(gs, EPI_ARGMAX);
   Epi ep = m->epi();
   ep.kind = EPI_ARGMAX; ep.R = Rl; ep.part = m->at<uint64_t>(L.w_lm); ep.part_stride = L.Rp;
   ep.logits = d_logits; ep.ldl = c.vocab;
   ep.row0 = lm == 2 ? R - 1 : 0;
   norm_in(ep, ss_a);
   PROF(JF_KERNEL_LMHEAD);
-  HIP_TRY(launch_gemm(dt, xn, pl_d, m->packed + L.p_lm, gs, ep, st));
+  int part_blocks = 0;
+  HIP_TRY(run_gemm(dt, Rl, c.vocab, d, xn, pl_d, m->packed + L.p_lm, ep, st, &part_blocks));
   PROF(JF_KERNEL_LMHEAD);
-  HIP_TRY(launch_argmax_reduce(ep.part, (int)gemm_blocks(gs), L.Rp, Rl, d_g, st));
+  HIP_TRY(launch_argmax_reduce(ep.part, part_blocks, L.Rp, Rl, d_g, st));
   return JF_OK;
 }
 
@@ -795,14 +821,13 @@ extern "C" jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t 
   if (R < 1 || R > 256) return fail(JF_E_CAPACITY, "R must be in [1, 256]");
   if (d < 128 || d % 128 || V < 16 || V % 16) return fail(JF_E_SHAPE, "d multiple of 128, V multiple of 16");
   hipStream_t st = (hipStream_t)stream;
-  GemmShape gs{R, V, d, 1, 1, 1};
-  gemm_plan(gs, EPI_ARGMAX);
-  gs.S = 1;  // no split-K scratch in the component call
   Epi ep{};
   ep.kind = EPI_ARGMAX; ep.R = R; ep.part = (uint64_t*)d_ws; ep.part_stride = R;
   ep.logits = d_logits; ep.ldl = V;
-  HIP_TRY(launch_gemm(dtype, d_x, (size_t)(R + 15) / 16 * 16 * d, d_w_packed, gs, ep, st));
-  HIP_TRY(launch_argmax_reduce(ep.part, (int)gemm_blocks(gs), R, R, d_argmax, st));
+  int part_blocks = 0;
+  // no split-K scratch in the component call
+  HIP_TRY(run_gemm(dtype, R, V, d, d_x, (size_t)(R + 15) / 16 * 16 * d, d_w_packed, ep, st, &part_blocks, false));
+  HIP_TRY(launch_argmax_reduce(ep.part, part_blocks, R, R, d_argmax, st));
   if (d_draft) {
     int32_t* zero = (int32_t*)((char*)d_ws + (size_t)(V / 16) * R * 8);
     HIP_TRY(launch_set_int(zero, 0, st));

@@ -94,6 +94,29 @@ hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
                        const GemmShape& s, const Epi& ep, hipStream_t stream);
 size_t gemm_blocks(const GemmShape& s);
 
+// Many-row GEMM (gemm_mr.hip), bf16, R > 32, wide matrices only: 8-wave
+// workgroups, each wave all row tiles of a chunk x its own column tiles,
+// over LDS-staged activations.
+struct MrPlan {
+  int R;            // rows (> 32)
+  int A;            // row tiles per half chunk (2, 4): 32 A rows per chunk
+  int B;            // column tiles per wave at most
+  int KC;           // 128-wide K-blocks
+  int P;            // pack group of the weight matrix
+  int T;            // 16-column tiles of N
+  int gr;           // column tiles per unit (2: SwiGLU pairs)
+  int n_cg;         // column groups (workgroups along N)
+  int passes;       // column passes per group
+  int S;            // K splits (1)
+  int chunks;       // row chunks of 32 A rows
+};
+int mr_row_tiles_half(int R);
+// false if the shape is not for this kernel
+bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus);
+size_t gemm_mr_lds_bytes(const MrPlan& m);
+hipError_t launch_gemm_mr(const void* X, size_t xplane, const void* Wp, const MrPlan& m, const Epi& ep,
+                          hipStream_t stream);
+
 // Packs W[rows][cols] (row-major) into the kernels' block layout, reading
 // source row rowmap[i] (or i if rowmap is null) from one of up to 4 source
 // matrices: rowmap entries are (src << 24) | row.
