@@ -1,15 +1,15 @@
-// Many-row GEMM of the decoder's wide projections (gate/up and the LM
-// head), Y[R][N] = X[R][K] * W[N][K]^T, for the wide Jacobi steps:
-// multi-block drafts with recycled candidates (Sec. 3.2, App. A Alg. 1), the
-// packed training forward and the block-size sweeps: 33 .. 64 rows in one
-// chunk, more as 128-row chunks.
+// Column-slice GEMM of the decoder's projections, Y[R][N] = X[R][K] *
+// W[N][K]^T, for the wide Jacobi steps (more than 32 rows: multi-block
+// drafts with recycled candidates, Sec. 3.2 and App. A Alg. 1; the packed
+// training forward; the block-size sweeps): the wide projections (gate/up,
+// LM head) and the long-K narrow one (down).  Rows go in chunks of 64 or 128.
 //
 // What bounds these launches is the bytes each compute unit requests (its
 // share of the weights plus the activations it re-reads), so the kernel asks
-// for every weight byte exactly once per compute unit and re-reads the
-// activations as rarely as the register file allows:
+// for every weight byte exactly once per compute unit and for the
+// activations once per pass:
 //   * a workgroup of 8 waves owns a column group (one pass of up to 8B
-//     16-column tiles; wider groups take several passes) and all K;
+//     16-column tiles; wider groups take several passes) and a K-range;
 //   * the activations of all the chunk's rows for half a 128-wide K-block
 //     (2 of its 4 fragment steps) are staged in LDS, double-buffered, and
 //     read by every wave; each wave multiplies all row tiles by its own
@@ -20,9 +20,12 @@
 //     same depth in step with them (the counter of outstanding loads retires
 //     them in issue order, so a stage's activations must not queue behind
 //     later weights); the workgroup barrier that hands over an LDS stage
-//     waits only for LDS traffic.
+//     waits only for LDS traffic;
+//   * split K (long-K narrow matrices): each workgroup writes its raw
+//     partial tile and a second kernel sums the partials in split order
+//     (deterministic) and runs the epilogue.
 // Epilogues are those of the weight-streaming kernel (jf_epilogue.h), run on
-// an LDS tile one row half at a time.
+// an LDS tile.
 #include <algorithm>
 
 #include "jf_device.h"
@@ -50,13 +53,18 @@ __device__ __forceinline__ void split_units(int u0, int u1, int n, int p, int gr
 }
 
 // Stage h of a pass (K-block kb0 + h / 2, fragment steps 2 (h % 2), + 1) of
-// the chunk's 2A row tiles x 2 planes: A 16-byte pieces per thread.
-template <int A>
-__device__ __forceinline__ void mr_load_act(u32x4_t (&stg)[A], const bf16_t* __restrict__ xrow, size_t xplane, int KC,
-                                            int kb0, int rtiles, int h) {
+// the chunk's RT row tiles x 2 planes, 256 RT 16-byte pieces: RT / 2 a
+// thread.
+template <int RT> constexpr int mr_pieces() {
+  static_assert(RT % 2 == 0, "an even number of row tiles");
+  return 256 * RT / kMrThreads;
+}
+template <int RT>
+__device__ __forceinline__ void mr_load_act(u32x4_t (&stg)[mr_pieces<RT>()], const bf16_t* __restrict__ xrow,
+                                            size_t xplane, int KC, int kb0, int rtiles, int h) {
   const int kb = kb0 + (h >> 1), jh = h & 1;
 #pragma unroll
-  for (int i = 0; i < A; ++i) {
+  for (int i = 0; i < mr_pieces<RT>(); ++i) {
     const int e = threadIdx.x + kMrThreads * i;              // 16-byte piece of the stage
     const int rt = e >> 8, pl = (e >> 7) & 1, q = e & 127;   // row tile, plane, piece of the 2 KB half
     const int rtc = min(rt, rtiles - 1);
@@ -64,11 +72,11 @@ __device__ __forceinline__ void mr_load_act(u32x4_t (&stg)[A], const bf16_t* __r
                                                (size_t)jh * 1024 + q * 8);
   }
 }
-template <int A>
-__device__ __forceinline__ void mr_store_act(const u32x4_t (&stg)[A], bf16_t* lbuf) {
+template <int RT>
+__device__ __forceinline__ void mr_store_act(const u32x4_t (&stg)[mr_pieces<RT>()], bf16_t* lbuf) {
   u32x4_t* dst = reinterpret_cast<u32x4_t*>(lbuf);
 #pragma unroll
-  for (int i = 0; i < A; ++i) dst[threadIdx.x + kMrThreads * i] = stg[i];
+  for (int i = 0; i < mr_pieces<RT>(); ++i) dst[threadIdx.x + kMrThreads * i] = stg[i];
 }
 // The wave's weight fragments of stage h: B tiles x 2 fragment steps.
 template <int B>
@@ -81,13 +89,13 @@ __device__ __forceinline__ void mr_load_w(Frag<bf16_t> (&w)[B][2], const bf16_t*
     for (int jj = 0; jj < 2; ++jj) w[t][jj] = frag_load<bf16_t>(wb[t] + off + jj * 512);
 }
 // acc[r][t] += rows (row tile r of the chunk, from the LDS stage) x weights
-// (tile t), for all 2A row tiles.
-template <int A, int B>
-__device__ __forceinline__ void mr_compute(f32x4_t (&acc)[2 * A][B], const bf16_t* la, const Frag<bf16_t> (&w)[B][2]) {
+// (tile t), for all RT row tiles.
+template <int RT, int B>
+__device__ __forceinline__ void mr_compute(f32x4_t (&acc)[RT][B], const bf16_t* la, const Frag<bf16_t> (&w)[B][2]) {
 #pragma unroll
   for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-    for (int r = 0; r < 2 * A; ++r) {
+    for (int r = 0; r < RT; ++r) {
       ActFrag<bf16_t> x;
       x.hi.v = *reinterpret_cast<const uint4*>(la + (size_t)(r * 2 + 0) * 1024 + jj * 512);
       x.lo.v = *reinterpret_cast<const uint4*>(la + (size_t)(r * 2 + 1) * 1024 + jj * 512);
@@ -96,36 +104,36 @@ __device__ __forceinline__ void mr_compute(f32x4_t (&acc)[2 * A][B], const bf16_
     }
 }
 
-constexpr int kStageElems(int A) { return 2 * A * 2 * 1024; }  // 2A row tiles x 2 planes x 1024 bf16
+constexpr int kStageElems(int RT) { return RT * 2 * 1024; }  // RT row tiles x 2 planes x 1024 bf16
 
 // The K loop of one pass over nst half-K-block stages.  kW: the wave has
 // column tiles (else it only stages activations and keeps the barriers in
 // step).  Straight-line prologue and steady state, so that the compiler's
 // count of outstanding loads stays exact and both rings stay in flight.
-template <int A, int B, int D, bool kW>
-__device__ __forceinline__ void mr_kloop(f32x4_t (&acc)[2 * A][B], const bf16_t* __restrict__ xrow, size_t xplane,
+template <int RT, int B, int D, bool kW>
+__device__ __forceinline__ void mr_kloop(f32x4_t (&acc)[RT][B], const bf16_t* __restrict__ xrow, size_t xplane,
                                          int KC, int kb0, int rtiles, int nst, const bf16_t* const (&wb)[B],
                                          size_t kstride, bf16_t* lact, const bf16_t* lane_lds) {
-  constexpr int SE = kStageElems(A);
+  constexpr int SE = kStageElems(RT);
   Frag<bf16_t> wr[D][B][2];
-  u32x4_t ar[D][A];
+  u32x4_t ar[D][mr_pieces<RT>()];
   // a pass shorter than the ring re-reads its last stage
 #pragma unroll
   for (int d = 0; d < D; ++d) {
-    mr_load_act<A>(ar[d], xrow, xplane, KC, kb0, rtiles, min(d, nst - 1));
+    mr_load_act<RT>(ar[d], xrow, xplane, KC, kb0, rtiles, min(d, nst - 1));
     if constexpr (kW) mr_load_w<B>(wr[d], wb, kstride, min(d, nst - 1));
   }
-  mr_store_act<A>(ar[0], lact);
+  mr_store_act<RT>(ar[0], lact);
   lds_barrier();
   int hb = 0;
   for (; hb + 2 * D <= nst; hb += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int h = hb + d;
-      if constexpr (kW) mr_compute<A, B>(acc, lane_lds + (size_t)(h & 1) * SE, wr[d]);
-      mr_load_act<A>(ar[d], xrow, xplane, KC, kb0, rtiles, h + D);
+      if constexpr (kW) mr_compute<RT, B>(acc, lane_lds + (size_t)(h & 1) * SE, wr[d]);
+      mr_load_act<RT>(ar[d], xrow, xplane, KC, kb0, rtiles, h + D);
       if constexpr (kW) mr_load_w<B>(wr[d], wb, kstride, h + D);
-      mr_store_act<A>(ar[(d + 1) % D], lact + (size_t)((h + 1) & 1) * SE);
+      mr_store_act<RT>(ar[(d + 1) % D], lact + (size_t)((h + 1) & 1) * SE);
       lds_barrier();
     }
   }
@@ -134,53 +142,57 @@ __device__ __forceinline__ void mr_kloop(f32x4_t (&acc)[2 * A][B], const bf16_t*
   for (int d = 0; d < 2 * D; ++d) {
     const int h = hb + d;
     if (h < nst) {
-      if constexpr (kW) mr_compute<A, B>(acc, lane_lds + (size_t)(h & 1) * SE, wr[d % D]);
+      if constexpr (kW) mr_compute<RT, B>(acc, lane_lds + (size_t)(h & 1) * SE, wr[d % D]);
       if (h + D < nst) {
-        mr_load_act<A>(ar[d % D], xrow, xplane, KC, kb0, rtiles, h + D);
+        mr_load_act<RT>(ar[d % D], xrow, xplane, KC, kb0, rtiles, h + D);
         if constexpr (kW) mr_load_w<B>(wr[d % D], wb, kstride, h + D);
       }
-      if (h + 1 < nst) mr_store_act<A>(ar[(d + 1) % D], lact + (size_t)((h + 1) & 1) * SE);
+      if (h + 1 < nst) mr_store_act<RT>(ar[(d + 1) % D], lact + (size_t)((h + 1) & 1) * SE);
       lds_barrier();
     }
   }
 }
 
-template <int A, int B, int D>
+// Row tiles per epilogue round: the LDS tile holds ER x 16 rows of a pass.
+constexpr int mr_epi_tiles(int RT) { return RT / 2; }
+
+template <int RT, int B, int D>
 __global__ void __launch_bounds__(kMrThreads, 1)
 k_gemm_mr(const bf16_t* __restrict__ X, size_t xplane, const bf16_t* __restrict__ Wp, MrPlan m, Epi ep) {
+  constexpr int ER = mr_epi_tiles(RT);
   extern __shared__ float lds[];
   bf16_t* lact = reinterpret_cast<bf16_t*>(lds);           // two activation stages
-  __shared__ float s_rs[16 * A];
+  __shared__ float s_rs[16 * ER];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int g = blockIdx.x, z = blockIdx.z;
+  const int g = blockIdx.x, sk = blockIdx.y, z = blockIdx.z;
   const int KC = m.KC, P = m.P;
   // rows of this chunk
-  const int r0 = z * 32 * A;
-  const int Rz = min(32 * A, m.R - r0);
+  const int r0 = z * 16 * RT;
+  const int Rz = min(16 * RT, m.R - r0);
   const int rtiles = (Rz + 15) / 16;                       // valid row tiles
   const int U = m.T / m.gr;
   const int u0 = (int)(((long)U * g) / m.n_cg), u1 = (int)(((long)U * (g + 1)) / m.n_cg);
   const int np = m.passes;
   const size_t kstride = (size_t)P * kBlockElems;
-  const int nst = 2 * KC;                                  // half-K-block stages of a pass
+  const int kb0 = (KC * sk) / m.S, kb1 = (KC * (sk + 1)) / m.S;
+  const int nst = 2 * (kb1 - kb0);                         // half-K-block stages of a pass
 
-  // the pass's column tiles [pl, ph); wave w takes tiles pl + B w .. (up to
-  // B of them), so every wave but one has B tiles or none
-  auto pass_tiles = [&](int p, int& pl, int& ph) { split_units(u0, u1, np, p, m.gr, pl, ph); };
   auto toff = [&](int t) { return ((size_t)(t / P) * KC * P + t % P) * kBlockElems; };
 
   const bf16_t* xrow = X + ((size_t)(r0 / 16) * KC << 11);  // the chunk's first row tile
   // the other RMSNorm accumulator (filled by the next producer) is cleared
   // by the first workgroup, as in the weight-streaming kernel
-  if (ep.ss_clear && g == 0 && z == 0)
+  if (ep.ss_clear && g == 0 && sk == 0 && z == 0)
     for (int i = threadIdx.x; i < 3 * ep.ss_stride; i += kMrThreads)
       __hip_atomic_store(ep.ss_clear + i, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
-  f32x4_t acc[2 * A][B];
+  f32x4_t acc[RT][B];
   const bf16_t* lane_lds = lact + lane * 8;
   for (int p = 0; p < np; ++p) {
+    // the pass's column tiles [pl, ph); wave w takes tiles pl + B w .. (up
+    // to B of them), so every wave but one has B tiles or none
     int pl, ph;
-    pass_tiles(p, pl, ph);
+    split_units(u0, u1, np, p, m.gr, pl, ph);
     const int c_lo = pl + B * wave;
     const int nb = max(0, min(B, ph - c_lo));              // wave-uniform
     // a partly filled wave re-reads its last tile in the empty slots (an L2
@@ -188,34 +200,45 @@ k_gemm_mr(const bf16_t* __restrict__ X, size_t xplane, const bf16_t* __restrict_
     const bf16_t* wb[B];
 #pragma unroll
     for (int t = 0; t < B; ++t)
-      wb[t] = Wp + toff(min(c_lo + min(t, max(nb - 1, 0)), m.T - 1)) + lane * 8;
+      wb[t] = Wp + toff(min(c_lo + min(t, max(nb - 1, 0)), m.T - 1)) + (size_t)kb0 * kstride + lane * 8;
 #pragma unroll
-    for (int r = 0; r < 2 * A; ++r)
+    for (int r = 0; r < RT; ++r)
 #pragma unroll
       for (int t = 0; t < B; ++t) acc[r][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (nb > 0)
-      mr_kloop<A, B, D, true>(acc, xrow, xplane, KC, 0, rtiles, nst, wb, kstride, lact, lane_lds);
+      mr_kloop<RT, B, D, true>(acc, xrow, xplane, KC, kb0, rtiles, nst, wb, kstride, lact, lane_lds);
     else
-      mr_kloop<A, B, D, false>(acc, xrow, xplane, KC, 0, rtiles, nst, wb, kstride, lact, lane_lds);
+      mr_kloop<RT, B, D, false>(acc, xrow, xplane, KC, kb0, rtiles, nst, wb, kstride, lact, lane_lds);
 
-    // epilogue through an LDS tile aliased over the activation stages, one
-    // row half (16 A rows) at a time
+    // epilogue through an LDS tile aliased over the activation stages, ER
+    // row tiles at a time; with split K the tile goes out raw, row-major per
+    // split, for the reduction kernel
     const int cols = (ph - pl) * 16, tld = cols + 1;
+    const int N = m.T * 16;
     float* tile = lds;
-    for (int half = 0; half < 2; ++half) {
-      const int hr0 = r0 + half * 16 * A;
-      const int hR = min(16 * A, m.R - hr0);
+    for (int er = 0; er < RT / ER; ++er) {
+      const int hr0 = r0 + er * 16 * ER;
+      const int hR = min(16 * ER, m.R - hr0);
       if (hR <= 0) break;                                  // block-uniform
       __syncthreads();
 #pragma unroll
-      for (int i = 0; i < A; ++i)
+      for (int i = 0; i < ER; ++i)
 #pragma unroll
         for (int t = 0; t < B; ++t)
           if (t < nb)
 #pragma unroll
             for (int k = 0; k < 4; ++k)
               tile[(i * 16 + 4 * (lane >> 4) + k) * tld + (c_lo - pl + t) * 16 + (lane & 15)] =
-                  acc[half * A + i][t][k];
+                  acc[er * ER + i][t][k];
+      if (m.S > 1) {
+        __syncthreads();
+        float* kp = ep.kpart + ((size_t)sk * m.R + hr0) * N + pl * 16;
+        for (int e = threadIdx.x; e < hR * cols; e += kMrThreads) {
+          const int r = e / cols, c = e - r * cols;
+          kp[(size_t)r * N + c] = tile[r * tld + c];
+        }
+        continue;
+      }
       if (ep.ss_in)
         for (int r = threadIdx.x; r < hR; r += kMrThreads) {
           uint64_t w[3];
@@ -235,13 +258,64 @@ k_gemm_mr(const bf16_t* __restrict__ X, size_t xplane, const bf16_t* __restrict_
   }
 }
 
-// ---- plans ------------------------------------------------------------------------
-int mr_row_tiles_half(int R) {
-  // above 128 rows: 128-row chunks (each re-reads the weights, but a wider
-  // chunk leaves registers for one column tile a wave, and re-reading the
-  // activations once per 8 tiles costs more)
-  return R <= 64 ? 2 : 4;
+// Split-K reduction: block (x, y) sums the S partials of rows 16 y .. and
+// columns 64 x .. in split order (deterministic), applies the folded RMSNorm
+// and runs the epilogue (its per-block argmax slot is x).  Each thread owns
+// 4 adjacent columns of one row and keeps 8 partial loads in flight.
+constexpr int kRedRows = 16, kRedCols = 64, kRedThreads = 256;
+
+__global__ void __launch_bounds__(kRedThreads) k_mr_reduce(MrPlan m, Epi ep) {
+  constexpr int tld = kRedCols + 1;
+  __shared__ float tile[kRedRows * tld];
+  __shared__ float s_rs[kRedRows];
+  const int N = m.T * 16;
+  const int c0 = blockIdx.x * kRedCols, r0 = blockIdx.y * kRedRows;
+  const int cols = min(kRedCols, N - c0), rows = min(kRedRows, m.R - r0);
+  const size_t split = (size_t)m.R * N;
+  if (ep.ss_in && threadIdx.x < rows) {
+    uint64_t w[3];
+    ss_load(ep.ss_in, ep.ss_stride, r0 + threadIdx.x, w);
+    s_rs[threadIdx.x] = ss_rstd(w, ep.norm_inv_d, ep.norm_eps);
+  }
+  __syncthreads();
+  const int r = threadIdx.x / (kRedCols / 4), c = 4 * (threadIdx.x % (kRedCols / 4));
+  float4 v = {0.f, 0.f, 0.f, 0.f};
+  if (r < rows && c < cols) {                               // cols is a multiple of 16
+    const float4* p = reinterpret_cast<const float4*>(ep.kpart + (size_t)(r0 + r) * N + c0 + c);
+    const size_t sp = split / 4;
+    int s = 0;
+    for (; s + 8 <= m.S; s += 8) {
+      float4 x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = p[(size_t)(s + j) * sp];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) { v.x += x[j].x; v.y += x[j].y; v.z += x[j].z; v.w += x[j].w; }
+    }
+    float4 x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (s + j < m.S) x[j] = p[(size_t)(s + j) * sp];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (s + j < m.S) { v.x += x[j].x; v.y += x[j].y; v.z += x[j].z; v.w += x[j].w; }
+    if (ep.ss_in) {
+      const float k = s_rs[r];
+      v.x *= k; v.y *= k; v.z *= k; v.w *= k;
+    }
+  }
+  tile[r * tld + c + 0] = v.x;
+  tile[r * tld + c + 1] = v.y;
+  tile[r * tld + c + 2] = v.z;
+  tile[r * tld + c + 3] = v.w;
+  __syncthreads();
+  epilogue<bf16_t>(tile, tld, cols, c0, ep, blockIdx.x, threadIdx.x, kRedThreads, r0, rows);
 }
+
+// ---- plans ------------------------------------------------------------------------
+// Row tiles of a chunk: 64- and 128-row chunks (above 128 rows each chunk
+// re-reads the weights, but a wider chunk leaves registers for one column
+// tile a wave, and re-reading the activations once per 8 tiles costs more).
+int mr_row_tiles(int R) { return R <= 64 ? 4 : 8; }
 
 // Most column tiles one pass of a group holds (groups of ceil(U / n_cg)
 // units split into `passes` parts).
@@ -251,78 +325,130 @@ static long mr_max_pass_tiles(const MrPlan& m) {
   return (group + m.passes - 1) / m.passes * m.gr;
 }
 
-// Column tiles per wave that the register file holds next to the rings, per
-// row-tile count: accumulators 4 x 2A x B, weight ring 8 x B x D and
-// activation ring 4 x A x D registers a lane (D = 2), within the 256 of a
+// Column tiles per wave that the register file holds, per row-tile count:
+// accumulators 4 RT B, weight ring 8 B D and activation ring 2 D RT
+// registers a lane (ring depth D = 2 half K-blocks), within the 256 of a
 // wave at two waves per SIMD (checked: no spills).
-static int mr_max_cols(int A) { return A <= 2 ? 4 : 2; }
+static int mr_max_cols(int RT) { return RT == 4 ? 4 : 2; }
 
-bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus) {
+// Plan cost, in compute-unit clocks: a workgroup's requested bytes (its
+// weights, the activations of its K-range once per pass at half weight, as
+// they come from L2, and its partial sums) at the rate one compute unit
+// sustains on the weight streams (about 27 GB/s, 11 bytes a clock), or its
+// matrix / LDS work if larger, times the rounds of workgroups; split K adds
+// the reduction's traffic spread over the chip and its launch.
+static double mr_cost(const MrPlan& m, int cus) {
+  const double rows = std::min(m.R, 16 * m.RT);
+  const double tiles = (double)mr_max_pass_tiles(m) * m.passes;
+  const double kc = (m.KC + m.S - 1) / m.S;
+  double bytes = tiles * kc * 4096 + m.passes * rows * kc * 256;
+  if (m.S > 1) bytes += rows * tiles * 64;
+  const double stages = 2.0 * kc * m.passes;
+  const double work = stages * std::max(128.0 * m.RT * m.B, 256.0 * m.RT);
+  const double rounds = std::ceil((double)m.n_cg * m.S * m.chunks / cus);
+  double cost = rounds * std::max(bytes / 11.0, work);
+  if (m.S > 1) cost += ((double)m.S + 1) * m.R * m.T * 64 / cus / 11.0 + 12000.0;
+  return cost;
+}
+
+bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int max_splits) {
+  // Up to 32 rows the weight-streaming kernel is faster on every 7B-shaped
+  // projection: both run at the weight stream's rate per compute unit, and
+  // its many small workgroups balance the chip better than one workgroup
+  // per compute unit with a whole number of column tiles (measured: gate/up
+  // 50.5 against 52.9 us, LM head 169 against 222 us at 16 rows).
   if (R <= 32 || N % 16 || K % 128) return false;
-  const int A = mr_row_tiles_half(R);
+  const int RT = mr_row_tiles(R);
   m.R = R;
-  m.A = A;
+  m.RT = RT;
   m.KC = K / 128;
   m.P = pack_group(N);
   m.T = N / 16;
   m.gr = epi_kind == EPI_SWIGLU ? 2 : 1;
   if (m.T % m.gr) return false;
-  m.chunks = (R + 32 * A - 1) / (32 * A);
-  m.S = 1;
+  m.chunks = (R + 16 * RT - 1) / (16 * RT);
   const int U = m.T / m.gr;
-  const int per_chunk = std::max(1, std::max(1, n_cus) / m.chunks);  // workgroups per row chunk
-  // only matrices wide enough to give every compute unit a full wave's
-  // worth of columns; narrower ones stay on the weight-streaming kernel
-  if (m.T < 8 * per_chunk) return false;
-  m.n_cg = std::min(per_chunk, U);
-  // the fewest passes (each re-reads the activations), then the fewest tiles
-  // a wave that holds a pass (idle waves fetch nothing)
-  m.B = mr_max_cols(A);
-  m.passes = 1;
-  while (mr_max_pass_tiles(m) > 8L * m.B) ++m.passes;
-  m.B = (int)((mr_max_pass_tiles(m) + 7) / 8);
+  const int cus = std::max(1, n_cus);
+  const int per_chunk = std::max(1, cus / m.chunks);       // workgroups per row chunk in one round
+  // Measured on the 7B-shaped projections (64 and 192 rows): a matrix too
+  // narrow to give every compute unit a wave's worth of columns needs split
+  // K here, which pays (partials, a reduction launch) only over a long K
+  // (down: 64 K-blocks and more); short-K narrow matrices (QKV, O) run
+  // faster on the weight-streaming kernel's row chunks, and wide ones
+  // (gate/up, LM head) faster without split K.
+  const bool narrow = m.T < 8 * per_chunk;
+  if (narrow && m.KC < 64) return false;
+  if (!narrow) max_splits = 1;
+  double best = -1;
+  MrPlan t = m;
+  for (int S = 1; S <= std::min(m.KC, std::min(max_splits, 64)); ++S) {
+    if (S > 1 && (size_t)S * R * N > kGemmPartFloats) break;
+    t.S = S;
+    t.n_cg = std::min(U, std::max(1, per_chunk / S));
+    // the fewest passes (each re-reads the activations), then the fewest
+    // tiles a wave that holds a pass (idle waves fetch nothing)
+    t.B = mr_max_cols(RT);
+    t.passes = 1;
+    while (mr_max_pass_tiles(t) > 8L * t.B) ++t.passes;
+    t.B = (int)((mr_max_pass_tiles(t) + 7) / 8);
+    const double c = mr_cost(t, cus);
+    if (best < 0 || c < best) {
+      best = c;
+      m = t;
+    }
+  }
   return true;
 }
 
 size_t gemm_mr_lds_bytes(const MrPlan& m) {
-  const size_t stages = (size_t)2 * kStageElems(m.A) * 2;                  // bytes
+  const size_t stages = (size_t)2 * kStageElems(m.RT) * 2;                  // bytes
   const int max_cols = 8 * m.B * 16;
-  const size_t tile = (size_t)16 * m.A * (max_cols + 1) * 4;
+  const size_t tile = (size_t)16 * mr_epi_tiles(m.RT) * (max_cols + 1) * 4;
   return std::max(stages, tile);
 }
 
-template <int A, int B, int D>
+template <int RT, int B>
 static hipError_t launch_mr_t(const void* X, size_t xplane, const void* Wp, const MrPlan& m, const Epi& ep,
                               hipStream_t st) {
-  hipLaunchKernelGGL((k_gemm_mr<A, B, D>), dim3(m.n_cg, 1, m.chunks), dim3(kMrThreads), gemm_mr_lds_bytes(m), st,
+  constexpr int D = 2;
+  hipLaunchKernelGGL((k_gemm_mr<RT, B, D>), dim3(m.n_cg, m.S, m.chunks), dim3(kMrThreads), gemm_mr_lds_bytes(m), st,
                      reinterpret_cast<const bf16_t*>(X), xplane, reinterpret_cast<const bf16_t*>(Wp), m, ep);
+  if (m.S > 1)
+    hipLaunchKernelGGL(k_mr_reduce, dim3(gemm_mr_part_blocks(m), (m.R + kRedRows - 1) / kRedRows), dim3(kRedThreads),
+                       0, st, m, ep);
   return hipGetLastError();
 }
 
-template <int A>
+template <int RT>
 static hipError_t launch_mr_b(const void* X, size_t xplane, const void* Wp, const MrPlan& m, const Epi& ep,
                               hipStream_t st) {
   switch (m.B) {
-    case 1: return launch_mr_t<A, 1, 2>(X, xplane, Wp, m, ep, st);
-    case 2: return launch_mr_t<A, 2, 2>(X, xplane, Wp, m, ep, st);
-    case 3: if constexpr (A <= 2) return launch_mr_t<A, 3, 2>(X, xplane, Wp, m, ep, st); break;
-    case 4: if constexpr (A <= 2) return launch_mr_t<A, 4, 2>(X, xplane, Wp, m, ep, st); break;
+    case 1: return launch_mr_t<RT, 1>(X, xplane, Wp, m, ep, st);
+    case 2: return launch_mr_t<RT, 2>(X, xplane, Wp, m, ep, st);
+    case 3: if constexpr (RT == 4) return launch_mr_t<RT, 3>(X, xplane, Wp, m, ep, st); break;
+    case 4: if constexpr (RT == 4) return launch_mr_t<RT, 4>(X, xplane, Wp, m, ep, st); break;
     default: break;
   }
   return hipErrorInvalidValue;
 }
 
+int gemm_mr_part_blocks(const MrPlan& m) {
+  return m.S > 1 ? (m.T * 16 + kRedCols - 1) / kRedCols : m.n_cg * m.passes;
+}
+
 hipError_t launch_gemm_mr(const void* X, size_t xplane, const void* Wp, const MrPlan& m, const Epi& ep,
                           hipStream_t st) {
-  if (m.R <= 32 || m.T < 1 || m.KC < 1 || m.n_cg < 1 || m.S != 1 || m.passes < 1 || m.gr < 1 || m.B < 1 ||
-      m.B > mr_max_cols(m.A) || m.T % m.gr || m.chunks != (m.R + 32 * m.A - 1) / (32 * m.A) || ep.row0 != 0)
+  if (m.R < 1 || m.T < 1 || m.KC < 1 || m.n_cg < 1 || m.S < 1 || m.S > m.KC || m.passes < 1 || m.gr < 1 || m.B < 1 ||
+      m.RT != mr_row_tiles(m.R) || m.B > mr_max_cols(m.RT) || m.T % m.gr ||
+      m.chunks != (m.R + 16 * m.RT - 1) / (16 * m.RT) || ep.row0 != 0)
     return hipErrorInvalidValue;
   // every pass must fit the waves' column tiles (8 waves of at most B)
   if (mr_max_pass_tiles(m) > 8L * m.B) return hipErrorInvalidValue;
   if (gemm_mr_lds_bytes(m) > 160 * 1024) return hipErrorInvalidValue;
-  switch (m.A) {
-    case 2: return launch_mr_b<2>(X, xplane, Wp, m, ep, st);
+  if (m.S > 1 && (!ep.kpart || (size_t)m.S * m.R * m.T * 16 > kGemmPartFloats)) return hipErrorInvalidValue;
+  switch (m.RT) {
     case 4: return launch_mr_b<4>(X, xplane, Wp, m, ep, st);
+    case 8: return launch_mr_b<8>(X, xplane, Wp, m, ep, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -383,18 +383,18 @@ static int device_cus() {
   return cus > 0 ? cus : 256;
 }
 
-// One projection Y[R][N] = X[R][K] W^T with epilogue ep: the many-row kernel
-// (gemm_mr.hip) for bf16 with more than 32 rows, else the weight-streaming
+// One projection Y[R][N] = X[R][K] W^T with epilogue ep: the column-slice
+// kernel (gemm_mr.hip) for bf16 where its plan takes the shape (more than
+// 32 rows: wide matrices and long-K narrow ones), else the weight-streaming
 // kernel.  *part_blocks (if not null) gets the number of per-row argmax key
 // slots the launch writes (EPI_ARGMAX).  split_k = false keeps K in one
 // workgroup (callers without split-K scratch).
 static hipError_t run_gemm(int dtype, int R, int N, int K, const void* X, size_t xplane, const void* W, const Epi& ep,
                            hipStream_t st, int* part_blocks = nullptr, bool split_k = true) {
-  if (dtype == JF_BF16 && R > 32 && ep.row0 == 0) {
+  if (dtype == JF_BF16 && ep.row0 == 0) {
     MrPlan mp{};
-    if (gemm_mr_plan(mp, R, N, K, ep.kind, device_cus())) {
-      if (!split_k) mp.S = 1;
-      if (part_blocks) *part_blocks = mp.n_cg * mp.passes;
+    if (gemm_mr_plan(mp, R, N, K, ep.kind, device_cus(), split_k ? 64 : 1)) {
+      if (part_blocks) *part_blocks = gemm_mr_part_blocks(mp);
       return launch_gemm_mr(X, xplane, W, mp, ep, st);
     }
   }

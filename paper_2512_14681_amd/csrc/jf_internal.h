@@ -94,12 +94,13 @@ hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
                        const GemmShape& s, const Epi& ep, hipStream_t stream);
 size_t gemm_blocks(const GemmShape& s);
 
-// Many-row GEMM (gemm_mr.hip), bf16, R > 32, wide matrices only: 8-wave
-// workgroups, each wave all row tiles of a chunk x its own column tiles,
-// over LDS-staged activations.
+// Column-slice GEMM (gemm_mr.hip), bf16: 8-wave workgroups, each wave all
+// row tiles of a chunk x its own column tiles, over LDS-staged activations
+// (requested once per compute unit); split K writes partials that a second
+// kernel reduces.
 struct MrPlan {
-  int R;            // rows (> 32)
-  int A;            // row tiles per half chunk (2, 4): 32 A rows per chunk
+  int R;            // rows
+  int RT;           // row tiles per chunk (4, 8): 16 RT rows per chunk
   int B;            // column tiles per wave at most
   int KC;           // 128-wide K-blocks
   int P;            // pack group of the weight matrix
@@ -107,13 +108,16 @@ struct MrPlan {
   int gr;           // column tiles per unit (2: SwiGLU pairs)
   int n_cg;         // column groups (workgroups along N)
   int passes;       // column passes per group
-  int S;            // K splits (1)
-  int chunks;       // row chunks of 32 A rows
+  int S;            // K splits (partials in Epi::kpart, S x R x N floats)
+  int chunks;       // row chunks of 16 RT rows
 };
-int mr_row_tiles_half(int R);
-// false if the shape is not for this kernel
-bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus);
+int mr_row_tiles(int R);
+// false if the shape is not for this kernel; max_splits 1: no split-K
+// scratch
+bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int max_splits);
 size_t gemm_mr_lds_bytes(const MrPlan& m);
+// per-block argmax slots (EPI_ARGMAX) the plan's epilogue writes
+int gemm_mr_part_blocks(const MrPlan& m);
 hipError_t launch_gemm_mr(const void* X, size_t xplane, const void* Wp, const MrPlan& m, const Epi& ep,
                           hipStream_t stream);
 
