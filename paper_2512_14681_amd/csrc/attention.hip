@@ -20,6 +20,8 @@
 // waves' (max, sum, O) states merge in LDS; with several splits each block
 // writes its partial state and k_attn_combine merges them in split order
 // (deterministic).
+#include <algorithm>
+
 #include "jf_device.h"
 #include "jf_internal.h"
 
@@ -355,6 +357,251 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   }
 }
 
+// ---- K/V pages shared through LDS (bf16, head_dim 128) ----------------------------
+// Block (kv head g, query group, key split): up to 8 query tiles of the KV
+// head, one per wave, over the split's keys.  Each 64-key page's K rows
+// (16 KB) and V^T rows (16 KB) are staged in LDS once per block and read by
+// every wave, so the keys are fetched once per query group instead of once
+// per query tile.  Pages stream through a register ring two pages deep into
+// two LDS buffers; the per-wave maths (S^T = K Q^T, online softmax, O^T +=
+// V^T P^T, Q and P as hi + lo bf16 terms) is that of k_attn.  Each wave owns
+// its query tile's state, so there is no merge across waves; with several
+// splits the states go to the combine kernel.
+//
+// LDS layout, in 16-byte slots, swizzled so that a fragment read touches 16
+// distinct bank groups per 16 lanes: K row r (a key) piece c at
+// 16 r + (c ^ kswz(r)); V^T row d (a dim) piece p (8 keys) at
+// 8 d + (p ^ ((d >> 1) & 7)).
+constexpr int kAttnLdsHD = 128;
+constexpr int kAttnLdsPieces = 16 * kAttnLdsHD / 512;  // 16-byte pieces a thread stages per page
+constexpr int kAttnLdsPageElems = 2 * kPage * kAttnLdsHD;
+
+__device__ __forceinline__ int kswz(int r) { return (r & 3) | (((r >> 3) & 3) << 2); }
+
+__global__ void __launch_bounds__(512, 1) k_attn_lds(AttnArgs a) {
+  constexpr int HD = kAttnLdsHD;
+  extern __shared__ float lds_raw[];
+  bf16_t* s_kv = reinterpret_cast<bf16_t*>(lds_raw);  // two pages: K (64 x HD) then V^T (HD x 64)
+  __shared__ int s_pt[kAttnMaxPages];
+  const int g = blockIdx.x, qgrp = blockIdx.y;
+  const int split = blockIdx.z, S = gridDim.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = a.H / a.G;
+  const int R = a.R;
+  const int nq = grp * R;
+  const int ntiles = (nq + 15) / 16;
+  const int tile = qgrp * a.qg + wave;
+  const bool active = wave < a.qg && tile < ntiles;     // wave-uniform
+  // this split's keys [k0, k1): whole pages, from the host's bound of C + R
+  int per = (a.keys_ub + S - 1) / S;
+  per = (per + kPage - 1) / kPage * kPage;
+  const int k0 = split * per;
+  const int k1 = min(a.keys_ub, k0 + per);
+  const int p0 = k0 / kPage;
+  const int np = k1 > k0 ? (k1 - 1) / kPage - p0 + 1 : 0;
+  for (int i = threadIdx.x; i < np; i += 512) s_pt[i] = a.page_table[p0 + i];
+  const int C = a.state ? a.state[0] : a.C_host;
+  const int lim = min(k1, C + R);                       // keys at or past lim are not visible here
+  const int npg = lim > k0 ? (lim - k0 + kPage - 1) / kPage : 0;  // pages with visible keys
+
+  const int ql = lane & 15, kg = lane >> 4;
+  const bf16_t* kv = reinterpret_cast<const bf16_t*>(a.kv);
+  const size_t page_elems = (size_t)2 * a.G * kPage * HD;
+  const size_t k_off = (size_t)g * kPage * HD;
+  const size_t vt_off = (size_t)a.G * kPage * HD + (size_t)g * HD * kPage;
+
+  ActFrag<bf16_t> qf[HD / 32];
+  uint64_t vw[4];
+  int r = 0, head = 0;
+  {
+    const int qr = tile * 16 + ql;
+    const bool qvalid = active && qr < nq;
+    const int hl = qvalid ? qr / R : 0;
+    r = qvalid ? qr - hl * R : 0;
+    head = g * grp + hl;
+    const bf16_t* qp = reinterpret_cast<const bf16_t*>(a.q) + ((size_t)r * a.H + head) * HD + 8 * kg;
+#pragma unroll
+    for (int c = 0; c < HD / 32; ++c) qf[c] = qvalid ? act_load<bf16_t>(qp + 32 * c, a.q_plane) : act_zero<bf16_t>();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (a.vis) {
+        vw[i] = a.vis[r * 4 + i];
+      } else {  // causal: rows 0..r
+        int lo = i * 64;
+        vw[i] = r < lo ? 0ull : (r - lo >= 63 ? ~0ull : ((2ull << (r - lo)) - 1ull));
+      }
+    }
+  }
+  __syncthreads();  // s_pt
+  {
+    // first use of the query fragments and masks ahead of the page loop, so
+    // that the compiler waits for their loads here: waited for inside the
+    // loop, their count would merge with the page ring's and drain it
+    uint32_t use = 0;
+#pragma unroll
+    for (int c = 0; c < HD / 32; ++c)
+      use |= qf[c].hi.v.x | qf[c].hi.v.y | qf[c].hi.v.z | qf[c].hi.v.w | qf[c].lo.v.x | qf[c].lo.v.y |
+             qf[c].lo.v.z | qf[c].lo.v.w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) use |= (uint32_t)vw[i] | (uint32_t)(vw[i] >> 32);
+    asm volatile("" ::"v"(use));
+  }
+
+  // page i of the split into ring registers (clamped: a short split re-reads
+  // its last page) and from there into LDS buffer b
+  auto load_page = [&](u32x4_t (&st)[kAttnLdsPieces], int i) {
+    const bf16_t* page = kv + (size_t)s_pt[min(i, np - 1)] * page_elems;
+#pragma unroll
+    for (int j = 0; j < kAttnLdsPieces; ++j) {
+      const int e = threadIdx.x + 512 * j;
+      const bf16_t* src = j < kAttnLdsPieces / 2 ? page + k_off + (size_t)e * 8
+                                                 : page + vt_off + (size_t)(e - 8 * HD) * 8;
+      st[j] = *reinterpret_cast<const u32x4_t*>(src);
+    }
+  };
+  auto store_page = [&](const u32x4_t (&st)[kAttnLdsPieces], int b) {
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(s_kv + (size_t)b * kAttnLdsPageElems);
+#pragma unroll
+    for (int j = 0; j < kAttnLdsPieces; ++j) {
+      const int e = threadIdx.x + 512 * j;
+      if (j < kAttnLdsPieces / 2) {
+        const int rr = e >> 4, c = e & 15;
+        dst[16 * rr + (c ^ kswz(rr))] = st[j];
+      } else {
+        const int ev = e - 8 * HD, d = ev >> 3, pc = ev & 7;
+        dst[8 * HD + 8 * d + (pc ^ ((d >> 1) & 7))] = st[j];
+      }
+    }
+  };
+
+  const float scale = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t o[HD / 16];
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // one 32-key half h of the page in LDS buffer b (keys kp0 + 32 h ..)
+  auto compute = [&](int b, int kp0, int h) {
+    const uint4* lk = reinterpret_cast<const uint4*>(s_kv + (size_t)b * kAttnLdsPageElems);
+    const uint4* lv = lk + 8 * HD;
+    Frag<bf16_t> kf[2][HD / 32], vf[HD / 16];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const int rr = 32 * h + 8 * (ql >> 2) + 4 * kt + (ql & 3);
+#pragma unroll
+      for (int cc = 0; cc < HD / 32; ++cc) kf[kt][cc].v = lk[16 * rr + ((kg + 4 * cc) ^ kswz(rr))];
+    }
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      const int d = dt * 16 + ql, pc = 4 * h + kg;
+      vf[dt].v = lv[8 * d + (pc ^ ((d >> 1) & 7))];
+    }
+    const int key0 = kp0 + 32 * h + 8 * kg;  // key of p[0]; p[e] is key0 + e
+    f32x4_t sc[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      f32x4_t sh = f32x4_t{0.f, 0.f, 0.f, 0.f}, sl = sh;
+#pragma unroll
+      for (int cc = 0; cc < HD / 32; ++cc) {
+        mfma(sh, kf[kt][cc], qf[cc].hi);
+        mfma(sl, kf[kt][cc], qf[cc].lo);
+      }
+      sc[kt] = sh + sl;
+    }
+    const uint32_t vis = low_bits8(lim - key0) & (low_bits8(C - key0) | vis_bits8(vw, key0 - C));
+    float p[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = kt * 4 + i;
+        const float v = ((vis >> e) & 1u) ? sc[kt][i] * scale : -INFINITY;
+        p[e] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+    float psum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      p[e] = __builtin_amdgcn_exp2f(p[e] - m_use);
+      psum += p[e];
+    }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    const PFrag<bf16_t> pf = pfrag<bf16_t>(p);
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) o[dt] *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.hi);
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) mfma(o[dt], vf[dt], pf.lo);
+  };
+
+  // pages through a two-deep register ring and two LDS buffers; waves
+  // without a query tile stage pages and keep the barriers in step
+  if (npg > 0) {
+    u32x4_t ring[2][kAttnLdsPieces];
+    load_page(ring[0], 0);
+    load_page(ring[1], 1);
+    store_page(ring[0], 0);
+    __syncthreads();
+    // two pages an iteration, so the ring slots are static, and no condition
+    // inside: the loads and stores run unconditionally (past the end: the
+    // split's last page again, unused), so the compiler's count of
+    // outstanding loads stays exact
+    int i = 0;
+    for (; i + 2 <= npg; i += 2) {
+#pragma unroll
+      for (int slot = 0; slot < 2; ++slot) {
+        if (active) {
+          compute(slot, k0 + (i + slot) * kPage, 0);
+          compute(slot, k0 + (i + slot) * kPage, 1);
+        }
+        load_page(ring[slot], i + slot + 2);
+        store_page(ring[slot ^ 1], slot ^ 1);
+        __syncthreads();
+      }
+    }
+    if (i < npg && active) {                               // an odd last page, in buffer 0
+      compute(0, k0 + i * kPage, 0);
+      compute(0, k0 + i * kPage, 1);
+    }
+  }
+  if (!active) return;
+
+  // the tile's state: (max, sum) per query, O^T columns per lane
+  float lr = l_run;
+  lr += __shfl_xor(lr, 16);
+  lr += __shfl_xor(lr, 32);
+  const int qr = tile * 16 + ql;
+  if (qr >= nq) return;
+  const size_t nrow = (size_t)R * a.H;
+  const size_t qidx = (size_t)r * a.H + head;
+  if (S == 1) {
+    const float inv = 1.f / lr;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        act_store<bf16_t>(reinterpret_cast<bf16_t*>(a.out) + act_offset(r, head * HD + dt * 16 + 4 * kg + i, a.H * HD),
+                          a.out_plane, o[dt][i] * inv);
+  } else {
+    float* op = a.o_part + ((size_t)split * nrow + qidx) * HD + 4 * kg;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt)
+      *reinterpret_cast<float4*>(op + dt * 16) = make_float4(o[dt][0], o[dt][1], o[dt][2], o[dt][3]);
+    if (kg == 0) {
+      a.ml_part[((size_t)split * nrow + qidx) * 2 + 0] = m_run;
+      a.ml_part[((size_t)split * nrow + qidx) * 2 + 1] = lr;
+    }
+  }
+}
+
 // Launch shape: key splits such that each of a block's 4 waves gets at most
 // kAttnChunksPerWave 32-key chunks (one memory round trip), at most
 // kAttnMaxSplits splits, and at most kAttnMaxPages - 2 pages per split.
@@ -365,7 +612,38 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 // than the halved key traffic saves.
 constexpr long kAttnQt2Work = 50000;
 
+// The LDS-shared form: query groups of up to 8 tiles (balanced), and key
+// splits of at least one page up to about 256 blocks in all.
+static void attn_lds_plan(AttnArgs& a) {
+  const int ntiles = ((a.H / a.G) * a.R + 15) / 16;
+  const int groups = (ntiles + 7) / 8;
+  a.qg = (ntiles + groups - 1) / groups;
+  const int pages = (a.keys_ub + kPage - 1) / kPage;
+  int s = (256 + a.G * groups - 1) / (a.G * groups);
+  s = std::min(s, pages);
+  const int min_s = (pages + kAttnMaxPages - 3) / (kAttnMaxPages - 2);
+  a.splits = std::max(1, std::min(kAttnMaxSplits, std::max(s, min_s)));
+}
+
+// The LDS-shared form from this many query tiles per KV head, or this much
+// (query tiles x keys) work.  Measured on the attention workloads (28 q / 4
+// kv heads of 128, us, one-tile form -> LDS-shared form): P = 512: n = 16
+// 12.8 -> 13.1, n = 64 17.2 -> 15.3; P = 2048: n = 16 15.0 -> 20.5, n = 32
+// 19.1 -> 21.9, n = 64 26.9 -> 21.2; P = 8192: n = 16 27.9 -> 27.0, n = 32
+// 35.5 -> 29.2, n = 64 47.7 -> 35.2; the n = 16 step's attention (C ~ 1100)
+// 14.1 -> 17.3.  With few query tiles the LDS-shared form needs many key
+// splits to spread the keys, and merging them costs more than sharing the
+// pages saves.
+constexpr int kAttnLdsTiles = 20;
+constexpr long kAttnLdsWork = 50000;
+
 void attn_plan(AttnArgs& a) {
+  a.qg = 0;
+  const long qtiles = ((long)(a.H / a.G) * a.R + 15) / 16;
+  if (a.lds_ok && a.hd == kAttnLdsHD && (qtiles >= kAttnLdsTiles || qtiles * a.keys_ub >= kAttnLdsWork)) {
+    attn_lds_plan(a);
+    return;
+  }
   const int chunks = (a.keys_ub + 31) / 32;
   a.waves = 4;
   int s = (chunks + kAttnChunksPerWave * a.waves - 1) / (kAttnChunksPerWave * a.waves);
@@ -374,7 +652,6 @@ void attn_plan(AttnArgs& a) {
   a.splits = s < 1 ? 1 : (s > kAttnMaxSplits ? kAttnMaxSplits : s);
   // Many query tiles over long prefixes: two query tiles per block share
   // each key chunk.
-  const long qtiles = ((long)(a.H / a.G) * a.R + 15) / 16;
   a.qt = qtiles >= 2 && qtiles * a.keys_ub >= kAttnQt2Work ? 2 : 1;
 }
 
@@ -434,7 +711,37 @@ static hipError_t launch_checked(int dtype, const AttnArgs& a, hipStream_t st) {
 // one of them.
 constexpr int kAttnQt2Blocks = 448;
 
+static hipError_t launch_attn_lds(const AttnArgs& a, hipStream_t st) {
+  if (a.R < 1 || a.R > 256 || a.splits < 1 || a.splits > kAttnMaxSplits || a.H % a.G || a.keys_ub < a.R ||
+      a.keys_ub > a.max_ctx || a.qg < 1 || a.qg > 8 || a.hd != kAttnLdsHD)
+    return hipErrorInvalidValue;
+  {
+    int per = (a.keys_ub + a.splits - 1) / a.splits;
+    per = (per + kPage - 1) / kPage * kPage;
+    if (per / kPage + 1 > kAttnMaxPages) return hipErrorInvalidValue;
+  }
+  if (a.splits > 1 && (!a.o_part || !a.ml_part)) return hipErrorInvalidValue;
+  const int ntiles = ((a.H / a.G) * a.R + 15) / 16;
+  const int groups = (ntiles + a.qg - 1) / a.qg;
+  hipLaunchKernelGGL(k_attn_lds, dim3(a.G, groups, a.splits), dim3(512),
+                     (size_t)2 * kAttnLdsPageElems * sizeof(bf16_t), st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  constexpr int HD = kAttnLdsHD;
+  const dim3 grid(a.G, ntiles, HD / 32);
+  if (a.splits <= 4)
+    hipLaunchKernelGGL((k_attn_combine<bf16_t, HD, 4>), grid, dim3(256), 0, st, a);
+  else if (a.splits <= 8)
+    hipLaunchKernelGGL((k_attn_combine<bf16_t, HD, 8>), grid, dim3(256), 0, st, a);
+  else if (a.splits <= 16)
+    hipLaunchKernelGGL((k_attn_combine<bf16_t, HD, 16>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_attn_combine<bf16_t, HD, 32>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
+  if (a.qg > 0) return dtype == 1 ? launch_attn_lds(a, st) : hipErrorInvalidValue;
   if (dtype == 1 && a.qt == 2) {
     AttnArgs b = a;
     const long pairs = ((long)((a.H / a.G) * a.R + 15) / 16 + 1) / 2;

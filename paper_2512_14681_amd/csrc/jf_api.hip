@@ -502,6 +502,7 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
     if (!fused) {
       AttnArgs a{};
       a.H = H; a.G = G; a.hd = hd; a.R = R; a.max_ctx = c.max_ctx; a.keys_ub = keys_ub;
+      a.lds_ok = dt == JF_BF16;
       attn_plan(a);
       a.q = m->ws + L.w_q; a.q_plane = pl_h; a.kv = m->kv_layer(l); a.page_table = m->at<int32_t>(L.w_pt);
       a.state = state; a.vis = m->at<uint64_t>(L.w_vis);
@@ -778,6 +779,7 @@ extern "C" jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t h
   AttnArgs a{};
   a.H = n_heads; a.G = n_kv_heads; a.hd = head_dim; a.R = R; a.max_ctx = C + R;
   a.keys_ub = C + R;
+  a.lds_ok = dtype == JF_BF16;
   attn_plan(a);
   a.q = d_q; a.q_plane = (size_t)R * n_heads * head_dim;
   a.kv = d_kv_layer; a.page_table = d_page_table; a.state = nullptr; a.C_host = C;

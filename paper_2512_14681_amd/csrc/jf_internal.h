@@ -155,6 +155,8 @@ struct AttnArgs {
   int splits;
   int waves;                 // waves per block (4)
   int qt;                    // query tiles per block (1 or 2)
+  int lds_ok;                // bf16 K/V: the plan may choose the LDS-shared kernel
+  int qg;                    // LDS-shared kernel: query tiles per block (0: not chosen)
   int keys_ub;               // host upper bound of C + R (<= max_ctx): the split layout
   const void* q;             // [R][H][hd] activation planes
   size_t q_plane;
@@ -168,7 +170,8 @@ struct AttnArgs {
   void* out;                 // [R][H*hd] activation planes, GEMM-input layout
   size_t out_plane;
 };
-// Sets a.waves and a.splits from a.keys_ub (and the head counts).
+// Sets a.waves, a.splits, a.qt and a.qg from a.keys_ub (and the head
+// counts): the LDS-shared kernel (qg > 0) where a.lds_ok and head_dim 128.
 void attn_plan(AttnArgs& a);
 constexpr int kAttnChunksPerWave = 2;  // 32-key chunks per wave
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t stream);
