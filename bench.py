@@ -122,6 +122,110 @@ def cpu_baseline(shape, n, C, tpf, budget_s=20.0):
 
 
 
+def host_info():
+    """CPU model, core counts and the BLAS numpy runs on (threadpoolctl)."""
+    import threadpoolctl
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = [{"api": i.get("internal_api"), "library": os.path.basename(i.get("filepath", "")),
+             "version": i.get("version"), "threads": i.get("num_threads")}
+            for i in threadpoolctl.threadpool_info() if i.get("user_api") == "blas"]
+    return {"cpu_model": model, "nproc": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0)),
+            "blas": blas}
+
+
+def cpu_oracle_configs(shape7b):
+    """The oracle on the other configurations, each a bounded sample timed
+    once on the host (a reported baseline, like cpu_baseline):
+      config 1: the tiny fp32 decoder's block Jacobi decode (n = 8, 64 tokens);
+      config 2: attention at P = 2048, n = 16 and P = 8192, n = 64;
+      config 3: the LM head [64, 3584] x [152064, 3584] in fp64, argmax and
+                the perturbed-draft acceptance;
+      config 5: one 192-row step of the 7B shape after 2048 cached positions
+                (weights of 2 layers reused across depth, random prefix K/V).
+    """
+    import numpy as np
+
+    import jf_inputs
+    from oracle import jacobi as ojac
+    from oracle.model import DecoderOracle
+    from oracle.numerics import bf16_bits_to_float, round_bf16
+    out = {}
+    # config 1
+    tiny = jf_inputs.MODEL_SHAPES["tiny"]
+    be = ojac.TransformerBackend(DecoderOracle(tiny, jf_inputs.model_weights(tiny, seed=0)))
+    prompt = jf_inputs.prompt(1, 32, tiny["vocab"])
+    t0 = time.perf_counter()
+    toks, acc = ojac.generate_jacobi(be, prompt, 8, 64, "block", pad_seed=2)
+    t = time.perf_counter() - t0
+    out["config1_tiny"] = {"sample": "the whole decode (64 tokens, fp64)", "iterations": len(acc),
+                           "s": round(t, 3), "us_per_iteration": round(t / len(acc) * 1e6, 1)}
+    # config 2
+    H, G, hd = 28, 4, 128
+    att = {}
+    for P, n in ((2048, 16), (8192, 64)):
+        S = P + n
+        K = bf16_bits_to_float(jf_inputs.normal(20 + P + n, 1, S * G * hd, dtype="bf16")).reshape(S, G, hd)
+        Vv = bf16_bits_to_float(jf_inputs.normal(20 + P + n, 2, S * G * hd, dtype="bf16")).reshape(S, G, hd)
+        q = bf16_bits_to_float(jf_inputs.normal(20 + P + n, 3, n * H * hd, dtype="bf16")).reshape(n, H, hd)
+        m = DecoderOracle(dict(n_layers=1, d_model=H * hd, n_heads=H, n_kv_heads=G, head_dim=hd, d_ffn=128,
+                               vocab=16, rope_base=10000.0, rms_eps=1e-6, dtype="f32"), {})
+        m.K[0], m.Vc[0] = K[:P], Vv[:P]
+        t0 = time.perf_counter()
+        m.attention(0, q, K[P:], Vv[P:], np.tri(n, dtype=bool))
+        att[f"P{P}_n{n}_us"] = round((time.perf_counter() - t0) * 1e6, 1)
+    out["config2_attention"] = dict(att, sample="one call per shape, fp64, vectorised definition")
+    # config 3
+    R, d, V = 64, 3584, 152064
+    w = bf16_bits_to_float(jf_inputs.normal(0, 3000, V * d, std=0.02, dtype="bf16"), np.float32).reshape(V, d)
+    x = bf16_bits_to_float(jf_inputs.normal(1000, 1, R * d, dtype="bf16")).reshape(R, d)
+    t0 = time.perf_counter()
+    z = np.empty((R, V))
+    for s0 in range(0, V, 16384):
+        z[:, s0:s0 + 16384] = x @ w[s0:s0 + 16384].astype(np.float64).T
+    g = np.argmax(z, axis=1)
+    draft = np.concatenate([[0], g[:-1]])
+    draft[R // 2] = (draft[R // 2] + 1) % V
+    ojac.accept_linear(list(draft), list(g))
+    t = time.perf_counter() - t0
+    out["config3_lm_head_accept"] = {"sample": "one call, fp64 product", "us": round(t * 1e6, 1)}
+    del w, z
+    # config 5
+    names = ["embed", "final_norm", "lm_head"] + [f"layers.{l}.{k}" for l in (0, 1) for k in
+                                                  ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm",
+                                                   "w_gate", "w_up", "w_down")]
+    wts = jf_inputs.model_weights(shape7b, seed=0, names=set(names))
+    wts = {k: bf16_bits_to_float(v, np.float32) for k, v in wts.items()}
+    C, Rm = 2048, 192
+    G7, hd7 = shape7b["n_kv_heads"], shape7b["head_dim"]
+    kv = round_bf16(jf_inputs.normal(9, 1, C * G7 * hd7).reshape(C, G7, hd7))
+    toks = jf_inputs.token_ids(9, 2, Rm, shape7b["vocab"])
+    t_layers = {}
+    for nl in (0, 2):          # the step without layers (embedding, final norm, LM head), then 2 layers
+        m = DecoderOracle(dict(shape7b, n_layers=nl), wts, compute=np.float32, row_invariant=False,
+                          cache_weights=False)
+        m.K = [kv] * nl
+        m.Vc = [kv] * nl
+        t0 = time.perf_counter()
+        m.forward(toks, C + np.arange(Rm), np.tri(Rm, dtype=bool))
+        t_layers[nl] = time.perf_counter() - t0
+    per_layer = (t_layers[2] - t_layers[0]) / 2
+    out["config5_step_r192"] = {
+        "sample": ("192 rows after 2048 cached positions (float32 BLAS with bf16 rounding points, random "
+                   "prefix K/V), timed without layers and with 2 of the 28 layers; the 28-layer step is "
+                   "scaled from those"),
+        "s_head": round(t_layers[0], 3), "s_per_layer": round(per_layer, 3),
+        "s_step_28_layers": round(t_layers[0] + shape7b["n_layers"] * per_layer, 3)}
+    return out
+
+
 def _bits(t):
     """A torch bf16 tensor's bit patterns as int16 (the ABI's bf16 storage)."""
     return t.contiguous().view(__import__("torch").int16)
@@ -630,7 +734,13 @@ def main():
     if not args.no_cpu_baseline:
         t2 = time.time()
         out["cpu_baseline"] = cpu_baseline(shape, n, args.prompt, tpf)
+        out["cpu_baseline"]["host"] = host_info()
         log(f"cpu baseline: {out['cpu_baseline']['s_per_step']:.2f} s/step ({time.time() - t2:.0f}s)")
+        if not args.headline_only:
+            t2 = time.time()
+            out["cpu_baseline"]["other_configs"] = cpu_oracle_configs(shape)
+            log(f"cpu oracle on configs 1, 2, 3, 5: {out['cpu_baseline']['other_configs']} "
+                f"({time.time() - t2:.0f}s)")
     print(json.dumps(out), flush=True)
 
 

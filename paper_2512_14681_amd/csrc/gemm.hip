@@ -202,7 +202,11 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     // Partials travel with device-coherent (agent-scope) stores and loads,
     // which bypass the per-XCD L2, so no L2 write-back / invalidate fence is
     // needed: the stores are complete (s_waitcnt) before the counter
-    // increment, and the last block reads them after seeing the count.
+    // increment, and the last block reads them after seeing the count.  A
+    // release / acquire pair on the counter would say the same in the C++
+    // memory model, but on gfx950 an agent-scope release writes back and an
+    // acquire invalidates the whole L2 of the XCD, which costs more than the
+    // split saves; the wait below is the one ordering the stores need.
     __shared__ int s_last;
     const int cols = NT * 16;
     const size_t unit_part = ((size_t)ng * C + z) * S;  // this chunk's S partial tiles
@@ -211,7 +215,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
       const int row = e / cols, c = e - row * cols;
       __hip_atomic_store(mine + e, tile[row * tld + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's stores are done
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stores are done
     __syncthreads();
     if (threadIdx.x == 0)
       s_last = __hip_atomic_fetch_add(ep.kcount + ng * C + z, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
