@@ -11,6 +11,14 @@
         whose name contains "copy" (a plain device copy of N bytes that the
         profiled program runs first, e.g. ``bench.py --copy-probe``).
 
+    python -m paper_2512_14681_amd.profiling step-mfma DIR --rows R --ctx C [--select REGEX]
+        MFMA load of every phase of the forwards in a --pmc run of
+        SQ_INSTS_VALU_MFMA_MOPS_BF16, SQ_VALU_MFMA_BUSY_CYCLES and
+        GRBM_GUI_ACTIVE (one pass): issued bf16 flops, the matrix cores' busy
+        fraction, and the algorithmic flops of R rows at committed length C;
+        forwards are kept when one of their kernels matches REGEX
+        (k_accept: the Jacobi steps; k_tree_packed: the packed forward).
+
     python -m paper_2512_14681_amd.profiling ceiling [--gib G] [--reps K]
         HBM rates that plain library kernels reach on the device (GPU
         required): a full read of a G GiB bf16 tensor (torch's sum, fp32
@@ -215,6 +223,100 @@ def step_traffic(fetch_dir, write_dir, copy_bytes, layers=28, algo=None):
     return "\n".join(lines)
 
 
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
+
+
+def _forwards_by_dispatch(directory, select):
+    """{counter: {phase: [values]}} and {phase: [durations ns]} over the
+    forwards of a --pmc run, each from its mask builder (k_tree*) to the
+    next, kept when one of its kernels matches the regex select."""
+    pat = re.compile(select)
+    by_id = {}
+    for r in _rows(directory, "counter_collection.csv"):
+        d = by_id.setdefault(int(r["dispatch_id"]), {"name": short_name(r["kernel_name"]), "c": {},
+                                                     "ns": int(r["end_timestamp"]) - int(r["start_timestamp"])})
+        d["c"][r["counter_name"]] = float(r["counter_value"])
+    forwards, cur = [], None
+    for did in sorted(by_id):
+        d = by_id[did]
+        if d["name"].startswith("k_tree"):
+            cur = []
+            forwards.append(cur)
+        if cur is not None:
+            cur.append(d)
+    return [f for f in forwards if any(pat.search(d["name"]) for d in f)]
+
+
+def _label_forward(f, layers):
+    gemm_phase = ("qkv", "o", "gateup", "down")
+    gi = 0
+    for d in f:
+        n = d["name"]
+        if n.startswith("k_gemm"):
+            lab = "lm_head" if gi == 4 * layers else gemm_phase[gi % 4]
+            gi += 1
+        elif n.startswith("k_mr_reduce"):
+            lab = "down_reduce" if gi % 4 == 0 and gi > 0 else "reduce"
+        elif n.startswith("k_attn_combine"):
+            lab = "attn_combine"
+        elif n.startswith("k_attn"):
+            lab = "attn"
+        else:
+            lab = re.sub(r"<.*", "", n)
+        yield lab, d
+
+
+def step_mfma(directory, select, rows, ctx, layers=28, clock_ghz=2.4, simds=1024, xcds=8):
+    """MFMA load of every phase of the forwards in a rocprofv3 --pmc run of
+    MFMA_COUNTERS: issued bf16 work (SQ_INSTS_VALU_MFMA_MOPS_BF16, 512 flops
+    a unit), the matrix cores' busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over
+    all SIMDs against GRBM_GUI_ACTIVE, which the CSV sums over the XCDs), and
+    the algorithmic flops of the phase (2 R N K for a projection, 4 R keys hd
+    H for attention at the committed length ctx)."""
+    d, F, V, H, G, hd = 3584, 18944, 152064, 28, 4, 128
+    algo = {"qkv": 2 * rows * (H + 2 * G) * hd * d, "o": 2 * rows * d * H * hd, "gateup": 2 * rows * 2 * F * d,
+            "down": 2 * rows * d * F, "lm_head": 2 * rows * V * d, "attn": 4 * rows * (ctx + rows) * hd * H}
+    per = {}
+    fw = _forwards_by_dispatch(directory, select)
+    for f in fw:
+        for lab, dd in _label_forward(f, layers):
+            p = per.setdefault(lab, {"n": 0, "ns": 0.0, "mops": 0.0, "busy": 0.0, "grbm": 0.0})
+            p["n"] += 1
+            p["ns"] += dd["ns"]
+            p["mops"] += dd["c"].get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+            p["busy"] += dd["c"].get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            p["grbm"] += dd["c"].get("GRBM_GUI_ACTIVE", 0.0)
+    lines = [f"{len(fw)} forwards matched {select!r}; per dispatch:", "",
+             "| phase | dispatches | us (counter run) | issued bf16 GFLOP | algorithmic GFLOP | issued / algorithmic "
+             "| issued TFLOP/s | MFMA busy |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    order = ["qkv", "attn", "attn_combine", "o", "gateup", "down", "down_reduce", "lm_head"]
+    tot = {"ns": 0.0, "mops": 0.0, "algo": 0.0, "busy": 0.0, "grbm": 0.0}
+    for lab in order + sorted(k for k in per if k not in order):
+        if lab not in per:
+            continue
+        p = per[lab]
+        n = p["n"]
+        us = p["ns"] / n / 1e3
+        gf = p["mops"] / n * 512 / 1e9
+        a = algo.get(lab)
+        busy = p["busy"] / (p["grbm"] / xcds * simds) if p["grbm"] else 0.0
+        tot["ns"] += p["ns"]
+        tot["mops"] += p["mops"]
+        tot["busy"] += p["busy"]
+        tot["grbm"] += p["grbm"]
+        if a:
+            tot["algo"] += a * n
+        lines.append(f"| {lab} | {n} | {us:.1f} | {gf:.1f} | {f'{a / 1e9:.1f}' if a else '—'} | "
+                     f"{f'{gf * 1e9 / a:.2f}' if a else '—'} | {gf / us * 1e3:.1f} | {busy:.3f} |")
+    nf = max(1, len(fw))
+    lines += ["", f"- per forward: {tot['ns'] / nf / 1e3:.1f} us in the counter run, "
+              f"{tot['mops'] * 512 / nf / 1e12:.3f} TFLOP issued, {tot['algo'] / nf / 1e12:.3f} TFLOP algorithmic, "
+              f"MFMA busy {tot['busy'] / (tot['grbm'] / xcds * simds) if tot['grbm'] else 0:.3f} "
+              f"(cycle-weighted over the forward's dispatches)"]
+    return "\n".join(lines)
+
+
 def ceiling(gib=2.0, reps=20, peak_tbs=8.0):
     import torch
     n = int(gib * (1 << 30)) // 2
@@ -316,6 +418,11 @@ def main(argv=None):
     stt.add_argument("--layers", type=int, default=28)
     stt.add_argument("--n", type=int, default=16, help="rows of the steps (for the algorithmic bytes)")
     stt.add_argument("--ctx", type=int, default=1024, help="committed length (for the attention bytes)")
+    sm = sub.add_parser("step-mfma", help="MFMA load of every phase of the forwards in a --pmc run")
+    sm.add_argument("dir")
+    sm.add_argument("--select", default="k_accept", help="regex: keep forwards with a matching kernel")
+    sm.add_argument("--rows", type=int, required=True)
+    sm.add_argument("--ctx", type=int, required=True, help="committed length the forwards attend over")
     c = sub.add_parser("ceiling")
     c.add_argument("--gib", type=float, default=2.0)
     c.add_argument("--reps", type=int, default=20)
@@ -327,6 +434,8 @@ def main(argv=None):
         print(library_gemms(a.rows, a.reps), flush=True)
     elif a.cmd == "ceiling":
         print(ceiling(a.gib, a.reps), flush=True)
+    elif a.cmd == "step-mfma":
+        print(step_mfma(a.dir, a.select, a.rows, a.ctx))
     elif a.cmd == "step-traffic":
         print(step_traffic(a.fetch, a.write, a.copy_bytes, a.layers, algo_bytes_7b(a.n, a.ctx)))
     elif a.cmd == "stats":

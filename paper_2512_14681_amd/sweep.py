@@ -18,6 +18,9 @@ On the 7B-shaped bf16 decoder (random-init weights, a random prompt):
   each iteration accepts k tokens.  Tokens/s at each k are reported next to
   the one-row (autoregressive) rate.
 
+* with --packed, the packed noisy/clean forward (8 + 8 blocks of 16 after
+  the prefix, noise-aware mask; App. C packing);
+
 * with --grid, the configuration grid of App. E on latency only: block size
   n x verification size v (entries verified in parallel, each n tokens) at
   K = 2 blocks; one step holds the real-active draft, v - 1 recycled
@@ -44,9 +47,10 @@ def main(argv=None):
     ap.add_argument("--prefix", type=int, default=1024)
     ap.add_argument("--rows", default="1,2,4,8,16,24,32,48,64,96,128,160,192,224,256")
     ap.add_argument("--cands", default="0,1,2,4,6,8,10,12,15")
-    ap.add_argument("--k", default="1,2,3,4,5,8")
+    ap.add_argument("--k", default="1,2,3,4,5,8", help="accepted tokens per iteration ('' : no emulation)")
     ap.add_argument("--reps", type=int, default=10)
     ap.add_argument("--grid", action="store_true", help="the (n, verification size) grid at K = 2")
+    ap.add_argument("--packed", action="store_true", help="also time the packed noisy/clean forward")
     ap.add_argument("--grid-n", default="8,16,32,64,128")
     ap.add_argument("--grid-v", default="1,2,4,8,12")
     args = ap.parse_args(argv)
@@ -134,14 +138,24 @@ def main(argv=None):
                 grid.append(dict(costs(R, us), n=n_, v=v))
                 log(f"grid n={n_} v={v} R={R}: {us:.1f} us")
 
-    # fixed fast-forward emulation
-    ks = [int(k) for k in args.k.split(",")]
+    packed = []
+    if args.packed:
+        # the packed noisy/clean forward (App. C packing, noise-aware mask): 8 +
+        # 8 blocks of 16 after the prefix, as bench.py's packed workload
+        d_pk = torch.as_tensor(jf_inputs.token_ids(8, 1, 256, V), device="cuda")
+        us = timed(lambda: model.jf_packed_forward(d_pk, 8, 16, jf.JF_MASK_NOISY_CONTEXT, d_arg), args.reps)
+        packed.append(dict(costs(256, us), blocks=8, n=16))
+        log(f"packed R=256: {us:.1f} us")
+
+    # fixed fast-forward emulation (none with --k '')
+    ks = [int(k) for k in args.k.split(",") if k]
     n, iters = 16, 12
-    need = max(ks) * iters + 1
-    dec.reset()
-    ar = dec.generate_ar(prompt, need)               # one-row steps: the greedy continuation
-    C0 = model.jf_kv_length()
     fixed = []
+    C0 = None
+    if ks:
+        dec.reset()
+        ar = dec.generate_ar(prompt, max(ks) * iters + 1)   # one-row steps: the greedy continuation
+        C0 = model.jf_kv_length()
     for k in ks:
         dec.reset()
         dec.prefill(prompt)
@@ -171,7 +185,7 @@ def main(argv=None):
         for f in fixed:
             f["speedup_vs_one_row_steps"] = round(f["tokens_s"] / (1e6 / ar_us), 3)
     out = {"workload": f"7B-shaped bf16 decoder, {P}-token prefix, random-init weights",
-           "linear": linear, "tree": tree, "fixed_tpf_block16": fixed, "config_grid_k2": grid,
+           "linear": linear, "tree": tree, "packed": packed, "fixed_tpf_block16": fixed, "config_grid_k2": grid,
            "note": f"one-row step {ar_us} us; C0 after greedy continuation {C0}"}
     print(json.dumps(out), flush=True)
 
