@@ -61,7 +61,7 @@ typedef enum { JF_F32 = 0, JF_BF16 = 1 } jf_dtype;
  * Limits: d_model, d_ffn multiples of 128, d_model <= 4096; head_dim in
  * {32, 64, 128};
  * n_heads * head_dim a multiple of 128; n_heads a multiple of n_kv_heads;
- * vocab a multiple of 16; 1 <= max_rows <= 256; max_ctx a multiple of 64. */
+ * vocab a multiple of 16; 1 <= max_rows <= JF_MAX_ROWS; max_ctx a multiple of 64. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
   float rope_base, rms_eps;
@@ -102,6 +102,10 @@ typedef struct {
 
 enum { JF_ROLE_RA = 0, JF_ROLE_CAND = 1, JF_ROLE_PSEUDO = 2 };
 #define JF_MAX_SEGMENTS 16
+/* Rows of one step at most, and the u64 words of a row's in-step visibility
+ * mask (bit j of word j / 64: in-step row j is visible). */
+#define JF_MAX_ROWS 512
+#define JF_VIS_WORDS 8
 
 /* Result of one step, written on the device (16 bytes). */
 typedef struct {
@@ -245,7 +249,7 @@ jf_status jf_profile_end(jf_model *m, double *total_ms, int32_t *launches);
  * 0..C+R-1 in one layer's paged cache d_kv_layer (layout as in
  * jf_model_load; slots beyond C+R in a used page must hold finite values),
  * with the page table d_page_table.  Row r sees positions [0, C) and
- * in-step position C + j iff bit j of d_vis[r][4] is set (d_vis NULL:
+ * in-step position C + j iff bit j of d_vis[r][JF_VIS_WORDS] is set (d_vis NULL:
  * j <= r, causal).  out: activation planes of the [R][n_heads * head_dim]
  * matrix in the GEMM-input layout (the O projection's input), Rp * n_heads *
  * head_dim elements per plane.  d_ws of at least jf_attention_ws_bytes(...). */

@@ -56,17 +56,35 @@ template <> __device__ __forceinline__ PFrag<float> pfrag<float>(const float* p)
 
 constexpr int kAttnMaxPages = 256;  // pages of one key split (LDS page-table copy)
 
-// Bits j0 .. j0 + 7 of a row's 256-bit in-step visibility mask (bits outside
-// [0, 256) read as 0), branch-free.
-__device__ __forceinline__ uint32_t vis_bits8(const uint64_t (&vw)[4], int j0) {
-  const int jc = min(max(j0, 0), 255);
+// Bits j0 .. j0 + 7 of a row's in-step visibility mask (kVisWords words;
+// bits outside [0, kMaxRows) read as 0), branch-free.
+__device__ __forceinline__ uint32_t vis_bits8(const uint64_t (&vw)[kVisWords], int j0) {
+  const int jc = min(max(j0, 0), kMaxRows - 1);
   const int wi = jc >> 6, sh = jc & 63;
-  const uint64_t lo = wi == 0 ? vw[0] : (wi == 1 ? vw[1] : (wi == 2 ? vw[2] : vw[3]));
-  const uint64_t hi = wi == 0 ? vw[1] : (wi == 1 ? vw[2] : (wi == 2 ? vw[3] : 0ull));
+  uint64_t lo = 0, hi = 0;
+#pragma unroll
+  for (int i = 0; i < kVisWords; ++i) {
+    lo = wi == i ? vw[i] : lo;
+    hi = wi + 1 == i ? vw[i] : hi;
+  }
   const uint64_t win = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
   uint32_t b = (uint32_t)win & 0xFFu;
   if (j0 < 0) b = j0 > -8 ? ((uint32_t)vw[0] << (-j0)) & 0xFFu : 0u;
-  return j0 >= 256 ? 0u : b;
+  return j0 >= kMaxRows ? 0u : b;
+}
+
+// The visibility words of in-step row r: from vis ([R][kVisWords]), or the
+// causal mask (rows 0..r) when vis is null.
+__device__ __forceinline__ void vis_words(const uint64_t* vis, int r, uint64_t (&vw)[kVisWords]) {
+#pragma unroll
+  for (int i = 0; i < kVisWords; ++i) {
+    if (vis) {
+      vw[i] = vis[(size_t)r * kVisWords + i];
+    } else {
+      const int lo = i * 64;
+      vw[i] = r < lo ? 0ull : (r - lo >= 63 ? ~0ull : ((2ull << (r - lo)) - 1ull));
+    }
+  }
 }
 
 // Low n bits set, n clamped to [0, 8].
@@ -116,7 +134,7 @@ __global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
   const size_t vt_off = (size_t)a.G * kPage * HD + (size_t)g * HD * kPage;
 
   ActFrag<T> qf[QT][HD / 32];
-  uint64_t vw[QT][4];
+  uint64_t vw[QT][kVisWords];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     const int qr = (tile0 + t) * 16 + ql;
@@ -127,15 +145,7 @@ __global__ void __launch_bounds__(256, 2) k_attn(AttnArgs a) {
     const T* qp = reinterpret_cast<const T*>(a.q) + ((size_t)r * a.H + head) * HD + 8 * kg;
 #pragma unroll
     for (int c = 0; c < HD / 32; ++c) qf[t][c] = qvalid ? act_load<T>(qp + 32 * c, a.q_plane) : act_zero<T>();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (a.vis) {
-        vw[t][i] = a.vis[r * 4 + i];
-      } else {  // causal: rows 0..r
-        int lo = i * 64;
-        vw[t][i] = r < lo ? 0ull : (r - lo >= 63 ? ~0ull : ((2ull << (r - lo)) - 1ull));
-      }
-    }
+    vis_words(a.vis, r, vw[t]);
   }
   __syncthreads();  // s_pt
 
@@ -411,7 +421,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_lds(AttnArgs a) {
   const size_t vt_off = (size_t)a.G * kPage * HD + (size_t)g * HD * kPage;
 
   ActFrag<bf16_t> qf[HD / 32];
-  uint64_t vw[4];
+  uint64_t vw[kVisWords];
   int r = 0, head = 0;
   {
     const int qr = tile * 16 + ql;
@@ -422,15 +432,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_lds(AttnArgs a) {
     const bf16_t* qp = reinterpret_cast<const bf16_t*>(a.q) + ((size_t)r * a.H + head) * HD + 8 * kg;
 #pragma unroll
     for (int c = 0; c < HD / 32; ++c) qf[c] = qvalid ? act_load<bf16_t>(qp + 32 * c, a.q_plane) : act_zero<bf16_t>();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (a.vis) {
-        vw[i] = a.vis[r * 4 + i];
-      } else {  // causal: rows 0..r
-        int lo = i * 64;
-        vw[i] = r < lo ? 0ull : (r - lo >= 63 ? ~0ull : ((2ull << (r - lo)) - 1ull));
-      }
-    }
+    vis_words(a.vis, r, vw);
   }
   __syncthreads();  // s_pt
   {
@@ -443,7 +445,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_lds(AttnArgs a) {
       use |= qf[c].hi.v.x | qf[c].hi.v.y | qf[c].hi.v.z | qf[c].hi.v.w | qf[c].lo.v.x | qf[c].lo.v.y |
              qf[c].lo.v.z | qf[c].lo.v.w;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) use |= (uint32_t)vw[i] | (uint32_t)(vw[i] >> 32);
+    for (int i = 0; i < kVisWords; ++i) use |= (uint32_t)vw[i] | (uint32_t)(vw[i] >> 32);
     asm volatile("" ::"v"(use));
   }
 
@@ -684,7 +686,7 @@ static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
 }
 
 static hipError_t launch_checked(int dtype, const AttnArgs& a, hipStream_t st) {
-  if (a.R < 1 || a.R > 256 || a.splits < 1 || a.splits > kAttnMaxSplits || a.H % a.G || a.keys_ub < a.R ||
+  if (a.R < 1 || a.R > kMaxRows || a.splits < 1 || a.splits > kAttnMaxSplits || a.H % a.G || a.keys_ub < a.R ||
       a.keys_ub > a.max_ctx)
     return hipErrorInvalidValue;
   // the LDS page-table copy must hold one split's pages
@@ -712,7 +714,7 @@ static hipError_t launch_checked(int dtype, const AttnArgs& a, hipStream_t st) {
 constexpr int kAttnQt2Blocks = 448;
 
 static hipError_t launch_attn_lds(const AttnArgs& a, hipStream_t st) {
-  if (a.R < 1 || a.R > 256 || a.splits < 1 || a.splits > kAttnMaxSplits || a.H % a.G || a.keys_ub < a.R ||
+  if (a.R < 1 || a.R > kMaxRows || a.splits < 1 || a.splits > kAttnMaxSplits || a.H % a.G || a.keys_ub < a.R ||
       a.keys_ub > a.max_ctx || a.qg < 1 || a.qg > 8 || a.hd != kAttnLdsHD)
     return hipErrorInvalidValue;
   {

@@ -464,7 +464,7 @@ static hipError_t launch_rt(const void* X, size_t xplane, const void* Wp, const 
 
 hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
                        const GemmShape& s, const Epi& ep, hipStream_t st) {
-  if (s.R < 1 || s.R > 256 || s.K < 128 || s.K % 128 || s.N < 16 * s.NT || s.N % (16 * s.NT))
+  if (s.R < 1 || s.R > kMaxRows || s.K < 128 || s.K % 128 || s.N < 16 * s.NT || s.N % (16 * s.NT))
     return hipErrorInvalidValue;
   if (s.C != (s.R > kChunkRows ? (s.R + kChunkRows - 1) / kChunkRows : 1)) return hipErrorInvalidValue;
   if (s.S < 1 || s.S > s.K / 128) return hipErrorInvalidValue;

@@ -73,7 +73,7 @@ jf_status check_config(const jf_config* c) {
   if (c->n_heads % c->n_kv_heads) return fail(JF_E_SHAPE, "n_heads must be a multiple of n_kv_heads");
   if ((c->n_heads * c->head_dim) % 128) return fail(JF_E_SHAPE, "n_heads * head_dim must be a multiple of 128");
   if (c->vocab % 16) return fail(JF_E_SHAPE, "vocab must be a multiple of 16");
-  if (c->max_rows < 1 || c->max_rows > 256) return fail(JF_E_SHAPE, "max_rows must be in [1, 256]");
+  if (c->max_rows < 1 || c->max_rows > kMaxRows) return fail(JF_E_SHAPE, "max_rows must be in [1, %d]", kMaxRows);
   if (c->max_ctx < 64 || c->max_ctx % 64) return fail(JF_E_SHAPE, "max_ctx must be a positive multiple of 64");
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return fail(JF_E_INVAL, "rms_eps / rope_base out of range");
   return JF_OK;
@@ -120,7 +120,7 @@ Layout make_layout(const jf_config& c) {
   L.w_g = off; off = align_up(off + Rp * 4);
   L.w_parent = off; off = align_up(off + Rp * 4);
   L.w_pos = off; off = align_up(off + Rp * 4);
-  L.w_vis = off; off = align_up(off + Rp * 4 * 8);
+  L.w_vis = off; off = align_up(off + Rp * kVisWords * 8);
   L.w_cos = off; off = align_up(off + (size_t)c.max_ctx * (c.head_dim / 2) * 4);
   L.w_sin = off; off = align_up(off + (size_t)c.max_ctx * (c.head_dim / 2) * 4);
   L.w_pt = off; off = align_up(off + (size_t)L.n_pages * 4);
@@ -677,6 +677,7 @@ extern "C" jf_status jf_multiblock_step(jf_model* m, const int32_t* d_tokens, in
   return JF_OK;
 }
 
+static_assert(kMaxRows == JF_MAX_ROWS && kVisWords == JF_VIS_WORDS, "row limits of jf.h");
 static_assert(kMaskNoisyContext == JF_MASK_NOISY_CONTEXT && kMaskCleanContext == JF_MASK_CLEAN_CONTEXT,
               "mask constants");
 
@@ -775,7 +776,7 @@ extern "C" jf_status jf_attention(int32_t n_heads, int32_t n_kv_heads, int32_t h
   if (dtype != JF_F32 && dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", dtype);
   if (n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads) return fail(JF_E_SHAPE, "bad head counts");
   if (head_dim != 32 && head_dim != 64 && head_dim != 128) return fail(JF_E_SHAPE, "head_dim must be 32, 64 or 128");
-  if (R < 1 || R > 256 || C < 0) return fail(JF_E_CAPACITY, "R must be in [1, 256] and C >= 0");
+  if (R < 1 || R > kMaxRows || C < 0) return fail(JF_E_CAPACITY, "R must be in [1, %d] and C >= 0", kMaxRows);
   AttnArgs a{};
   a.H = n_heads; a.G = n_kv_heads; a.hd = head_dim; a.R = R; a.max_ctx = C + R;
   a.keys_ub = C + R;
@@ -820,7 +821,7 @@ extern "C" jf_status jf_lm_head_accept(int32_t R, int32_t d, int32_t V, int32_t 
   if (!d_x || !d_w_packed || !d_argmax || !d_ws) return fail(JF_E_INVAL, "null pointer argument");
   if (d_draft && !d_result) return fail(JF_E_INVAL, "acceptance needs d_result");
   if (dtype != JF_F32 && dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", dtype);
-  if (R < 1 || R > 256) return fail(JF_E_CAPACITY, "R must be in [1, 256]");
+  if (R < 1 || R > kMaxRows) return fail(JF_E_CAPACITY, "R must be in [1, %d]", kMaxRows);
   if (d < 128 || d % 128 || V < 16 || V % 16) return fail(JF_E_SHAPE, "d multiple of 128, V multiple of 16");
   hipStream_t st = (hipStream_t)stream;
   Epi ep{};
@@ -876,7 +877,7 @@ extern "C" jf_status jf_lm_head_accept_noalloc(int32_t R, int32_t d, int32_t V, 
   if (!d_x || !d_w_packed || !d_argmax) return fail(JF_E_INVAL, "null pointer argument");
   if (d_draft && !d_result) return fail(JF_E_INVAL, "acceptance needs d_result");
   if (dtype != JF_F32 && dtype != JF_BF16) return fail(JF_E_DTYPE, "dtype %d unsupported", dtype);
-  if (R < 1 || R > 256) return fail(JF_E_CAPACITY, "R must be in [1, 256]");
+  if (R < 1 || R > kMaxRows) return fail(JF_E_CAPACITY, "R must be in [1, %d]", kMaxRows);
   if (d < 128 || d % 128 || V < 16 || V % 16) return fail(JF_E_SHAPE, "d multiple of 128, V multiple of 16");
   const size_t need = jf_lm_head_ws_bytes(R, V);
   if (need > JF_NOALLOC_SCRATCH_BYTES)

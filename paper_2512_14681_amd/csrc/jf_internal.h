@@ -7,6 +7,8 @@
 namespace jf {
 
 constexpr int kPage = 64;  // tokens per KV page
+constexpr int kMaxRows = 512;             // rows of one step (draft, candidates, prefill chunk)
+constexpr int kVisWords = kMaxRows / 64;  // u64 words of a row's in-step visibility mask
 
 // Packed weight layout: 16-row tiles are stored in groups of P (4 when the
 // row count allows, else 2, else 1), and inside a group K-block-major with

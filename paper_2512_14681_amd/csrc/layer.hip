@@ -346,7 +346,7 @@ __device__ bool attn_item(const SideArgs& a, int item, float* lds, int* s_ok) {
   const int hl = qvalid ? qr / R : 0;
   const int r = qvalid ? qr - hl * R : 0;
   const int head = g * grp + hl;
-  const uint64_t vw = a.vis ? a.vis[r * 4] : (r >= 63 ? ~0ull : ((2ull << r) - 1ull));
+  const uint64_t vw = a.vis ? a.vis[(size_t)r * kVisWords] : (r >= 63 ? ~0ull : ((2ull << r) - 1ull));
 
   // K rows of the two score tiles of a 32-key chunk (row i of tile kt is key
   // 8 (i / 4) + 4 kt + i % 4) and the V^T fragments of keys 8 kg .. 8 kg + 7

@@ -16,7 +16,7 @@ namespace jf {
 __device__ void tree_walk(const int32_t* par, int r, int R, const int32_t* state, int32_t* parent,
                           int32_t* pos, uint64_t* vis) {
   if (r >= R) return;
-  uint64_t w[4] = {0, 0, 0, 0};
+  uint64_t w[kVisWords] = {};
   int depth = 0;
   int x = r;
   w[x >> 6] |= 1ull << (x & 63);
@@ -27,12 +27,12 @@ __device__ void tree_walk(const int32_t* par, int r, int R, const int32_t* state
   }
   parent[r] = par[r];
   pos[r] = state[0] + depth;
-  for (int i = 0; i < 4; ++i) vis[r * 4 + i] = w[i];
+  for (int i = 0; i < kVisWords; ++i) vis[r * kVisWords + i] = w[i];
 }
 
-__global__ void k_tree(SegArgs sg, int R, const int32_t* state, int32_t* flags, int32_t* parent,
-                       int32_t* pos, uint64_t* vis) {
-  __shared__ int32_t par[256];
+__global__ void __launch_bounds__(kMaxRows) k_tree(SegArgs sg, int R, const int32_t* state, int32_t* flags,
+                                                   int32_t* parent, int32_t* pos, uint64_t* vis) {
+  __shared__ int32_t par[kMaxRows];
   const int r = threadIdx.x;
   if (r == 0 && flags) *flags = 0;  // flags are per step
   if (r < R) {
@@ -51,8 +51,8 @@ __global__ void k_tree(SegArgs sg, int R, const int32_t* state, int32_t* flags, 
 
 hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t* flags,
                        int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t st) {
-  if (R < 1 || R > 256) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_tree, dim3(1), dim3(256), 0, st, segs, R, state, flags, parent, pos, vis);
+  if (R < 1 || R > kMaxRows) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_tree, dim3(1), dim3(kMaxRows), 0, st, segs, R, state, flags, parent, pos, vis);
   return hipGetLastError();
 }
 
@@ -64,9 +64,10 @@ hipError_t launch_tree(const SegArgs& segs, int R, const int32_t* state, int32_t
 // (noisy-context mask) or of clean block i - 1 (clean-context mask).  Both
 // copies of block i get depths i n .. i n + n - 1, the block's own
 // positions.
-__global__ void k_tree_packed(int n_blocks, int n, int mask, const int32_t* state, int32_t* flags,
-                              int32_t* parent, int32_t* pos, uint64_t* vis) {
-  __shared__ int32_t par[256];
+__global__ void __launch_bounds__(kMaxRows) k_tree_packed(int n_blocks, int n, int mask, const int32_t* state,
+                                                          int32_t* flags, int32_t* parent, int32_t* pos,
+                                                          uint64_t* vis) {
+  __shared__ int32_t par[kMaxRows];
   const int R = 2 * n_blocks * n;
   const int r = threadIdx.x;
   if (r == 0 && flags) *flags = 0;
@@ -86,9 +87,9 @@ __global__ void k_tree_packed(int n_blocks, int n, int mask, const int32_t* stat
 
 hipError_t launch_tree_packed(int n_blocks, int n, int mask, const int32_t* state, int32_t* flags,
                               int32_t* parent, int32_t* pos, uint64_t* vis, hipStream_t st) {
-  if (n_blocks < 1 || n < 1 || 2 * n_blocks * n > 256) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_tree_packed, dim3(1), dim3(256), 0, st, n_blocks, n, mask, state, flags, parent, pos,
-                     vis);
+  if (n_blocks < 1 || n < 1 || 2 * n_blocks * n > kMaxRows) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_tree_packed, dim3(1), dim3(kMaxRows), 0, st, n_blocks, n, mask, state, flags, parent,
+                     pos, vis);
   return hipGetLastError();
 }
 
@@ -198,11 +199,11 @@ hipError_t launch_argmax_reduce(const uint64_t* part, int nblocks, int stride, i
 // ---- a8: greedy acceptance of a linear draft + next draft --------------------------
 // a = 1 + longest run of draft[k] == g[k-1]; pending = g[a-1]; next draft is
 // the Jacobi update g[a-1], g[a], ... padded (mode 1) with pad ids at C+a+i.
-__global__ void k_accept_linear(const int32_t* draft, const int32_t* g, int n, int mode,
+__global__ void __launch_bounds__(kMaxRows) k_accept_linear(const int32_t* draft, const int32_t* g, int n, int mode,
                                 uint64_t seed, int V, const int32_t* state, const int32_t* flags,
                                 int32_t* result, int32_t* next_draft) {
   __shared__ int32_t s_a;
-  __shared__ int32_t gs[256];
+  __shared__ int32_t gs[kMaxRows];
   const int t = threadIdx.x;
   if (t < n) gs[t] = g[t];
   if (t == 0) s_a = n;
@@ -228,7 +229,8 @@ __global__ void k_accept_linear(const int32_t* draft, const int32_t* g, int n, i
 hipError_t launch_accept_linear(const int32_t* draft, const int32_t* g, int n, int mode,
                                 uint64_t seed, int V, const int32_t* state, const int32_t* flags,
                                 int32_t* result, int32_t* next_draft, hipStream_t st) {
-  hipLaunchKernelGGL(k_accept_linear, dim3(1), dim3(256), 0, st, draft, g, n, mode, seed, V, state,
+  if (n < 1 || n > kMaxRows) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_accept_linear, dim3(1), dim3(kMaxRows), 0, st, draft, g, n, mode, seed, V, state,
                      flags, result, next_draft);
   return hipGetLastError();
 }

@@ -20,6 +20,8 @@ JF_OK, JF_E_INVAL, JF_E_SHAPE, JF_E_CAPACITY, JF_E_DTYPE, JF_E_HIP, JF_E_STATE =
 JF_F32, JF_BF16 = 0, 1
 JF_ROLE_RA, JF_ROLE_CAND, JF_ROLE_PSEUDO = 0, 1, 2
 JF_MAX_SEGMENTS = 16
+JF_MAX_ROWS = 512      # rows of one step at most
+JF_VIS_WORDS = 8       # u64 words of a row's in-step visibility mask
 JF_FLAG_BAD_TOKEN, JF_FLAG_CAPACITY, JF_FLAG_SYNC = 1, 2, 4
 JF_OPT_FUSED_ATTENTION = 1
 JF_MASK_NOISY_CONTEXT, JF_MASK_CLEAN_CONTEXT = 0, 1

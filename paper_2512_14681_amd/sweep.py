@@ -22,11 +22,11 @@ On the 7B-shaped bf16 decoder (random-init weights, a random prompt):
   the prefix, noise-aware mask; App. C packing);
 
 * with --grid, the configuration grid of App. E on latency only: block size
-  n x verification size v (entries verified in parallel, each n tokens) at
-  K = 2 blocks; one step holds the real-active draft, v - 1 recycled
-  n-token entries under its root and one pseudo-active block,
-  R = (v + 1) n rows.  Points beyond the engine's 256 rows are reported as
-  such.  Tokens/s needs the TPF of trained weights and is not reported.
+  n x verification size v (entries verified in parallel, each n tokens) x
+  concurrent blocks K; one step holds the real-active draft, v - 1 recycled
+  n-token entries under its root and K - 1 chained pseudo-active blocks,
+  R = (v + K - 1) n rows.  Points beyond the engine's 512 rows are reported
+  as such.  Tokens/s needs the TPF of trained weights and is not reported.
 
 Prints one JSON object (stdout); progress on stderr.
 """
@@ -49,10 +49,11 @@ def main(argv=None):
     ap.add_argument("--cands", default="0,1,2,4,6,8,10,12,15")
     ap.add_argument("--k", default="1,2,3,4,5,8", help="accepted tokens per iteration ('' : no emulation)")
     ap.add_argument("--reps", type=int, default=10)
-    ap.add_argument("--grid", action="store_true", help="the (n, verification size) grid at K = 2")
+    ap.add_argument("--grid", action="store_true", help="the (n, verification size, K) grid")
     ap.add_argument("--packed", action="store_true", help="also time the packed noisy/clean forward")
     ap.add_argument("--grid-n", default="8,16,32,64,128")
     ap.add_argument("--grid-v", default="1,2,4,8,12")
+    ap.add_argument("--grid-k", default="2", help="concurrent blocks K of the grid")
     args = ap.parse_args(argv)
 
     import numpy as np
@@ -66,14 +67,14 @@ def main(argv=None):
     V, P = shape["vocab"], args.prefix
     rows = [int(r) for r in args.rows.split(",")]
     t0 = time.time()
-    model = jf.Model(shape, jf_inputs.model_weights(shape, seed=0), max_rows=256,
+    model = jf.Model(shape, jf_inputs.model_weights(shape, seed=0), max_rows=jf.JF_MAX_ROWS,
                      max_ctx=((P + 512 + 63) // 64) * 64)
     dec = decode.Decoder(model)
     prompt = jf_inputs.prompt(1, P, V)
     p = dec.prefill(prompt)
     log(f"model ready ({time.time() - t0:.0f}s)")
     st = torch.cuda.current_stream()
-    Rmax = 256
+    Rmax = jf.JF_MAX_ROWS
     d_tok = torch.tensor([p] + [decode.pad_token(2, P + i, V) for i in range(1, Rmax)], dtype=torch.int32,
                          device="cuda")
     d_arg = torch.zeros(Rmax, dtype=torch.int32, device="cuda")
@@ -120,23 +121,28 @@ def main(argv=None):
 
     grid = []
     if args.grid:
-        for n_ in (int(x) for x in args.grid_n.split(",")):
-            for v in (int(x) for x in args.grid_v.split(",")):
-                R = (v + 1) * n_
-                if R > Rmax:
-                    grid.append({"n": n_, "v": v, "rows": R, "us": None, "note": "exceeds 256 rows"})
-                    continue
-                segs = [(0, n_, -1, jf.JF_ROLE_RA, 1)]
-                for c in range(v - 1):
-                    segs.append((n_ * (1 + c), n_, 0, jf.JF_ROLE_CAND, 0))
-                segs.append((n_ * v, n_, n_ - 1, jf.JF_ROLE_PSEUDO, 0))
-                if len(segs) > jf.JF_MAX_SEGMENTS:
-                    grid.append({"n": n_, "v": v, "rows": R, "us": None, "note": "more than 16 segments"})
-                    continue
-                us = timed(lambda: model.jf_multiblock_step(d_tok, R, segs, d_arg, d_seg, d_res, d_path),
-                           args.reps)
-                grid.append(dict(costs(R, us), n=n_, v=v))
-                log(f"grid n={n_} v={v} R={R}: {us:.1f} us")
+        for K in (int(x) for x in args.grid_k.split(",")):
+            for n_ in (int(x) for x in args.grid_n.split(",")):
+                for v in (int(x) for x in args.grid_v.split(",")):
+                    R = (v + K - 1) * n_
+                    if R > Rmax:
+                        grid.append({"n": n_, "v": v, "K": K, "rows": R, "us": None,
+                                     "note": f"exceeds {Rmax} rows"})
+                        continue
+                    segs = [(0, n_, -1, jf.JF_ROLE_RA, 1)]
+                    for c in range(v - 1):
+                        segs.append((n_ * (1 + c), n_, 0, jf.JF_ROLE_CAND, 0))
+                    for b in range(K - 1):                   # pseudo-active blocks, chained
+                        first = n_ * (v + b)
+                        segs.append((first, n_, n_ - 1 if b == 0 else first - 1, jf.JF_ROLE_PSEUDO, 0))
+                    if len(segs) > jf.JF_MAX_SEGMENTS:
+                        grid.append({"n": n_, "v": v, "K": K, "rows": R, "us": None,
+                                     "note": f"more than {jf.JF_MAX_SEGMENTS} segments"})
+                        continue
+                    us = timed(lambda: model.jf_multiblock_step(d_tok, R, segs, d_arg, d_seg, d_res, d_path),
+                               args.reps)
+                    grid.append(dict(costs(R, us), n=n_, v=v, K=K))
+                    log(f"grid K={K} n={n_} v={v} R={R}: {us:.1f} us")
 
     packed = []
     if args.packed:
@@ -185,7 +191,7 @@ def main(argv=None):
         for f in fixed:
             f["speedup_vs_one_row_steps"] = round(f["tokens_s"] / (1e6 / ar_us), 3)
     out = {"workload": f"7B-shaped bf16 decoder, {P}-token prefix, random-init weights",
-           "linear": linear, "tree": tree, "packed": packed, "fixed_tpf_block16": fixed, "config_grid_k2": grid,
+           "linear": linear, "tree": tree, "packed": packed, "fixed_tpf_block16": fixed, "config_grid": grid,
            "note": f"one-row step {ar_us} us; C0 after greedy continuation {C0}"}
     print(json.dumps(out), flush=True)
 

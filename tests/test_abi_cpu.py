@@ -59,7 +59,7 @@ def test_query_sizes_valid(L):
     ("n_kv_heads", 3, jf.JF_E_SHAPE),
     ("vocab", 1000, jf.JF_E_SHAPE),
     ("max_rows", 0, jf.JF_E_SHAPE),
-    ("max_rows", 257, jf.JF_E_SHAPE),
+    ("max_rows", jf.JF_MAX_ROWS + 1, jf.JF_E_SHAPE),
     ("max_ctx", 100, jf.JF_E_SHAPE),
     ("rms_eps", 0.0, jf.JF_E_INVAL),
 ])
@@ -86,14 +86,15 @@ def test_null_arguments_rejected_without_hip(L):
     assert L.jf_kv_truncate(None, 0, None) == jf.JF_E_INVAL
     assert L.jf_attention(4, 4, 48, 1, 0, 4, P(1), P(1), P(1), None, P(1), P(1), None) == jf.JF_E_SHAPE
     assert L.jf_attention(4, 4, 32, 5, 0, 4, P(1), P(1), P(1), None, P(1), P(1), None) == jf.JF_E_DTYPE
-    assert L.jf_attention(4, 4, 32, 1, 0, 300, P(1), P(1), P(1), None, P(1), P(1), None) == jf.JF_E_CAPACITY
+    assert L.jf_attention(4, 4, 32, 1, 0, jf.JF_MAX_ROWS + 1, P(1), P(1), P(1), None, P(1), P(1), None) == jf.JF_E_CAPACITY
     assert L.jf_pack_matrix(20, 128, 1, P(1), P(1), None) == jf.JF_E_SHAPE
     assert L.jf_lm_head_accept(4, 100, 1024, 1, P(1), P(1), None, P(1), None, None, P(1), None) == jf.JF_E_SHAPE
     assert L.jf_lm_head_accept(4, 128, 1024, 1, P(1), P(1), P(1), P(1), None, None, P(1), None) == jf.JF_E_INVAL
     # the allocation-free LM head: same checks, plus its fixed scratch capacity
     assert L.jf_lm_head_accept_noalloc(4, 100, 1024, 1, P(1), P(1), None, P(1), None, None, None) == jf.JF_E_SHAPE
     assert L.jf_lm_head_accept_noalloc(4, 128, 1024, 1, None, P(1), None, P(1), None, None, None) == jf.JF_E_INVAL
-    assert L.jf_lm_head_accept_noalloc(300, 128, 1024, 1, P(1), P(1), None, P(1), None, None, None) == jf.JF_E_CAPACITY
+    assert L.jf_lm_head_accept_noalloc(jf.JF_MAX_ROWS + 1, 128, 1024, 1, P(1), P(1), None, P(1), None, None,
+                                       None) == jf.JF_E_CAPACITY
     assert L.jf_lm_head_accept_noalloc(256, 3584, 152064, 1, P(1), P(1), None, P(1), None, None,
                                        None) == jf.JF_E_CAPACITY
     assert "scratch" in L.jf_last_error().decode()

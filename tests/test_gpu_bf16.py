@@ -157,3 +157,53 @@ def test_fused_attention_repeat_is_bitwise_deterministic(env):
         outs.append(d_log.cpu().numpy())
     env["model"].jf_model_set_option(jf.JF_OPT_FUSED_ATTENTION, 0)
     assert np.array_equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("cands,pseudo", [(3, 1), (7, 0)])
+def test_multiblock_step_beyond_256_rows(env, cands, pseudo):
+    """Steps of more than 256 rows: blocks of n = 64 with the real-active draft,
+    `cands` recycled 64-token candidates under its root and `pseudo` chained
+    pseudo-active blocks (App. A Alg. 1).  (3, 1) is the paper's chosen
+    multi-block point, block 64 x verification 4 at K = 2 (App. E): 320 rows;
+    (7, 0) is 512 rows, the engine's maximum.  Every row's logits against
+    the oracle, and the device's verification, winner and path from its own
+    argmax."""
+    import torch
+    from oracle import tree as otree
+    from paper_2512_14681_amd import jf
+    V, n = SHAPE["vocab"], 64
+    R = n * (1 + cands + pseudo)
+    model = jf.Model(SHAPE, env["w"], max_rows=jf.JF_MAX_ROWS, max_ctx=704)
+    from paper_2512_14681_amd import decode
+    dec = decode.Decoder(model)
+    p = dec.prefill(env["prompt"])
+    C = len(env["prompt"])
+    segs = [(0, n, -1, jf.JF_ROLE_RA, 1)]
+    for c in range(cands):
+        segs.append((n * (1 + c), n, 0, jf.JF_ROLE_CAND, 0))
+    for b in range(pseudo):
+        first = n * (1 + cands + b)
+        segs.append((first, n, n - 1 if b == 0 else first - 1, jf.JF_ROLE_PSEUDO, 0))
+    rng = np.random.default_rng(R)
+    tokens = [p] + [int(t) for t in rng.integers(0, V, R - 1)]
+    d_tok = torch.tensor(tokens, dtype=torch.int32, device="cuda")
+    d_arg = torch.zeros(R, dtype=torch.int32, device="cuda")
+    d_seg = torch.zeros(jf.JF_MAX_SEGMENTS, dtype=torch.int32, device="cuda")
+    d_res = torch.zeros(4, dtype=torch.int32, device="cuda")
+    d_path = torch.zeros(R, dtype=torch.int32, device="cuda")
+    d_log = torch.empty((R, V), dtype=torch.float32, device="cuda")
+    model.jf_multiblock_step(d_tok, R, segs, d_arg, d_seg, d_res, d_path, d_log)
+    z = d_log.cpu().numpy()
+    g = d_arg.cpu().numpy()
+    ora = DecoderOracle(SHAPE, env["w"])
+    ora.prefill(np.asarray(env["prompt"]))
+    osegs = [otree.Segment(*s) for s in segs]
+    parent, pos, vis = otree.build(osegs, R, C)
+    zo, _ = ora.forward(np.asarray(tokens), pos, vis)
+    err = np.abs(z - zo).max()
+    assert err < LOGIT_TOL, err
+    assert ((g == zo.argmax(1)) | (gaps(zo) < GAP_EXEMPT)).all()
+    m_dev = list(d_seg.cpu().numpy()[:len(segs)])
+    res = d_res.cpu().numpy()
+    assert m_dev == otree.verify(np.asarray(tokens), g, parent, osegs)
+    assert (res[1], [int(x) for x in d_path.cpu().numpy()[:res[0]]]) == otree.winner_path(osegs, m_dev, parent)

@@ -179,7 +179,7 @@ def run_attention(H, G, hd, dtype, C, R, seed, tree=False):
             vis[r, r] = True
             if parent[r] >= 0:
                 vis[r] |= vis[parent[r]]
-    words = np.zeros((R, 4), np.uint64)
+    words = np.zeros((R, jf.JF_VIS_WORDS), np.uint64)
     for r in range(R):
         for j in np.nonzero(vis[r])[0]:
             words[r, j // 64] |= np.uint64(1) << np.uint64(j % 64)
@@ -219,13 +219,13 @@ def check_attn(out, want, dtype):
 
 @pytest.mark.parametrize("H,G,hd,dtype", [(4, 4, 32, "f32"), (8, 2, 64, "bf16"), (28, 4, 128, "bf16"),
                                           (28, 4, 128, "f32")])
-@pytest.mark.parametrize("C,R", [(0, 1), (5, 16), (100, 17), (600, 64), (130, 200)])
+@pytest.mark.parametrize("C,R", [(0, 1), (5, 16), (100, 17), (600, 64), (130, 200), (40, 512)])
 def test_attention_small(H, G, hd, dtype, C, R):
     out, want = run_attention(H, G, hd, dtype, C, R, seed=C * 7 + R)
     check_attn(out, want, dtype)
 
 
-@pytest.mark.parametrize("R", [9, 64, 192])
+@pytest.mark.parametrize("R", [9, 64, 192, 320, 512])
 def test_attention_tree_mask(R):
     out, want = run_attention(28, 4, 128, "bf16", 300, R, seed=R, tree=True)
     check_attn(out, want, "bf16")
