@@ -48,8 +48,8 @@ import re
 import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-GEMM_SOURCES = ("paper_2512_14681_amd/csrc/gemm.hip", "paper_2512_14681_amd/csrc/jf_device.h",
-                "paper_2512_14681_amd/csrc/jf_internal.h")
+GEMM_SOURCES = ("paper_2512_14681_amd/csrc/gemm.hip", "paper_2512_14681_amd/csrc/jf_epilogue.h",
+                "paper_2512_14681_amd/csrc/jf_device.h", "paper_2512_14681_amd/csrc/jf_internal.h")
 
 
 def _rows(directory, suffix):
