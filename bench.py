@@ -360,7 +360,7 @@ def bench_tiny():
 
 def bench_window(model, dec, shape, n, prompt_len=1024, steps=10, warmup=3):
     import torch
-    from paper_2512_14681_amd import decode
+    from paper_2512_14681_amd import decode, jf
     import jf_inputs
     V = shape["vocab"]
     dec.reset()
@@ -371,9 +371,8 @@ def bench_window(model, dec, shape, n, prompt_len=1024, steps=10, warmup=3):
     d_res = torch.zeros((warmup + steps, 4), dtype=torch.int32, device="cuda")
     st = torch.cuda.current_stream()
 
-    def step(i):
-        model.jf_jacobi_step(d_draft, n, 1, 2, d_arg, d_res[i], d_draft)
-        model.jf_commit_kv(None, d_res[i])
+    def step(i):  # window step with its commit (one fused argmax / acceptance / commit launch)
+        model.jf_jacobi_step(d_draft, n, 1 | jf.JF_STEP_COMMIT, 2, d_arg, d_res[i], d_draft)
     for i in range(warmup):
         step(i)
     us = _time_calls(lambda i: step(warmup + i), steps, st)
@@ -649,9 +648,8 @@ def main():
     d_res = torch.zeros((total, 4), dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
 
-    def step(i):
-        model.jf_jacobi_step(d_draft, n, 1, seed, d_argmax, d_res[i], d_draft)
-        model.jf_commit_kv(None, d_res[i])
+    def step(i):  # window step with its commit (one fused argmax / acceptance / commit launch)
+        model.jf_jacobi_step(d_draft, n, 1 | jf.JF_STEP_COMMIT, seed, d_argmax, d_res[i], d_draft)
 
     for i in range(W):
         step(i)

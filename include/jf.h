@@ -169,7 +169,11 @@ jf_status jf_prefill(jf_model *m, const int32_t *d_tokens, int32_t n,
  * pad_id(pad_seed, C + a + i) = splitmix64(pad_seed ^ (pos * 0x9E3779B97F4A7C15)) % V.
  * d_next_draft may equal d_draft.  d_logits (optional, may be NULL) receives
  * the fp32 logits [n][V].  The cache rows C..C+n-1 are overwritten with the
- * draft's K/V; jf_commit_kv keeps the accepted ones. */
+ * draft's K/V; jf_commit_kv keeps the accepted ones.  mode | JF_STEP_COMMIT
+ * also commits them in the step (C += a, as jf_commit_kv(m, NULL, d_result,
+ * 0, ...) would; no jf_commit_kv follows such a step).  The vocabulary
+ * argmax reduction, the acceptance and that commit run in one launch. */
+#define JF_STEP_COMMIT 2
 jf_status jf_jacobi_step(jf_model *m, const int32_t *d_draft, int32_t n,
                          int32_t mode, uint64_t pad_seed, int32_t *d_argmax,
                          jf_step_result *d_result, int32_t *d_next_draft,

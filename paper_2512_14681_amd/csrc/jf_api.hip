@@ -412,8 +412,11 @@ static hipError_t run_gemm(int dtype, int R, int N, int K, const void* X, size_t
 struct PackedSpec {
   int n_blocks, n, mask;
 };
+// lm_parts (lm == 1): when not null, the argmax reduction is left to the
+// caller's fused tail, which gets the number of per-block key slots here.
 static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegArgs& sg, int lm,
-                         int32_t* d_g, float* d_logits, hipStream_t st, const PackedSpec* pk = nullptr) {
+                         int32_t* d_g, float* d_logits, hipStream_t st, const PackedSpec* pk = nullptr,
+                         int* lm_parts = nullptr) {
   const jf_config& c = m->cfg;
   const Layout& L = m->L;
   const int dt = c.dtype;
@@ -557,6 +560,10 @@ static jf_status forward(jf_model* m, const int32_t* d_tokens, int R, const SegA
   int part_blocks = 0;
   HIP_TRY(run_gemm(dt, Rl, c.vocab, d, xn, pl_d, m->packed + L.p_lm, ep, st, &part_blocks));
   PROF(JF_KERNEL_LMHEAD);
+  if (lm_parts) {
+    *lm_parts = part_blocks;
+    return JF_OK;
+  }
   HIP_TRY(launch_argmax_reduce(ep.part, part_blocks, L.Rp, Rl, d_g, st));
   return JF_OK;
 }
@@ -608,20 +615,29 @@ extern "C" jf_status jf_jacobi_step(jf_model* m, const int32_t* d_draft, int32_t
                                     int32_t* d_next_draft, float* d_logits, jf_stream stream) {
   if (!m || !d_draft || !d_argmax || !d_result || !d_next_draft)
     return fail(JF_E_INVAL, "null pointer argument");
-  if (mode != 0 && mode != 1) return fail(JF_E_INVAL, "mode must be 0 (block) or 1 (window)");
+  if (mode < 0 || mode > (1 | JF_STEP_COMMIT))
+    return fail(JF_E_INVAL, "mode must be 0 (block) or 1 (window), optionally | JF_STEP_COMMIT");
   if (m->C_ub == 0) return fail(JF_E_STATE, "empty cache: prefill the prompt first");
   hipStream_t st = (hipStream_t)stream;
   jf_status s = check_rows(m, n, st);
   if (s != JF_OK) return s;
+  const int commit = (mode & JF_STEP_COMMIT) ? 1 : 0;
   SegArgs sg{};
   sg.n = 1; sg.first[0] = 0; sg.nrows[0] = n; sg.attach[0] = -1; sg.role[0] = 0; sg.verify_from[0] = 1;
   PROF(JF_KERNEL_STEP);
-  s = forward(m, d_draft, n, sg, 1, d_argmax, d_logits, st);
+  int parts = 0;
+  s = forward(m, d_draft, n, sg, 1, d_argmax, d_logits, st, nullptr, &parts);
   if (s != JF_OK) return s;
-  HIP_TRY(launch_accept_linear(d_draft, d_argmax, n, mode, pad_seed, m->cfg.vocab, m->state(),
-                               m->flags(), reinterpret_cast<int32_t*>(d_result), d_next_draft, st));
+  HIP_TRY(launch_argmax_accept_linear(m->at<uint64_t>(m->L.w_lm), parts, m->L.Rp, d_draft, n, mode & 1, pad_seed,
+                                      m->cfg.vocab, m->state(), m->flags(), reinterpret_cast<int32_t*>(d_result),
+                                      d_next_draft, d_argmax, commit, m->cfg.max_ctx, st));
   PROF(JF_KERNEL_STEP);
-  m->last_rows = n;
+  if (commit) {
+    m->C_ub = std::min(m->C_ub + n, m->cfg.max_ctx);
+    m->last_rows = 0;
+  } else {
+    m->last_rows = n;
+  }
   m->last_tree = 0;
   return JF_OK;
 }
@@ -667,10 +683,12 @@ extern "C" jf_status jf_multiblock_step(jf_model* m, const int32_t* d_tokens, in
   s = check_rows(m, R, st);
   if (s != JF_OK) return s;
   PROF(JF_KERNEL_STEP);
-  s = forward(m, d_tokens, R, sg, 1, d_argmax, d_logits, st);
+  int parts = 0;
+  s = forward(m, d_tokens, R, sg, 1, d_argmax, d_logits, st, nullptr, &parts);
   if (s != JF_OK) return s;
-  HIP_TRY(launch_accept_tree(sg, d_tokens, d_argmax, m->at<int32_t>(m->L.w_parent), R, m->flags(),
-                             d_seg_accept, reinterpret_cast<int32_t*>(d_result), d_path, st));
+  HIP_TRY(launch_argmax_accept_tree(m->at<uint64_t>(m->L.w_lm), parts, m->L.Rp, sg, d_tokens, R,
+                                    m->at<int32_t>(m->L.w_parent), m->state(), m->flags(), d_seg_accept,
+                                    reinterpret_cast<int32_t*>(d_result), d_path, d_argmax, st));
   PROF(JF_KERNEL_STEP);
   m->last_rows = R;
   m->last_tree = 1;

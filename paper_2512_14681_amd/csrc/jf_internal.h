@@ -237,6 +237,17 @@ hipError_t launch_accept_tree(const SegArgs& segs, const int32_t* tokens, const 
                               const int32_t* parent, int R, const int32_t* flags,
                               int32_t* seg_accept, int32_t* result, int32_t* path,
                               hipStream_t stream);
+// The argmax reduction of the LM head's per-block keys, the acceptance and
+// (linear steps, commit != 0) the commit, in one launch; state[2] is its
+// counter (zero between launches).
+hipError_t launch_argmax_accept_linear(const uint64_t* part, int nblocks, int stride, const int32_t* draft, int n,
+                                       int mode, uint64_t seed, int V, int32_t* state, const int32_t* flags,
+                                       int32_t* result, int32_t* next_draft, int32_t* g, int commit, int max_ctx,
+                                       hipStream_t stream);
+hipError_t launch_argmax_accept_tree(const uint64_t* part, int nblocks, int stride, const SegArgs& segs,
+                                     const int32_t* tokens, int R, const int32_t* parent, int32_t* state,
+                                     const int32_t* flags, int32_t* seg_accept, int32_t* result, int32_t* path,
+                                     int32_t* g, hipStream_t stream);
 hipError_t launch_commit(int dtype, void* kv, int L, int n_pages, int G, int hd,
                          const int32_t* page_table, int32_t* state, const int32_t* path,
                          const int32_t* result, int max_commit, int fixed_count, int max_ctx,

@@ -236,27 +236,29 @@ hipError_t launch_accept_linear(const int32_t* draft, const int32_t* g, int n, i
 }
 
 // ---- a8 (tree): per-segment verification, winner and committed path ------------
-__global__ void k_accept_tree(SegArgs sg, const int32_t* tokens, const int32_t* g,
-                              const int32_t* parent, int R, const int32_t* flags,
-                              int32_t* seg_accept, int32_t* result, int32_t* path) {
-  __shared__ int32_t m[16];
+// gv: the rows' argmax (global memory after a launch boundary, or a copy in
+// LDS); m_sh: LDS scratch of JF_MAX_SEGMENTS counts.  Threads s < sg.n verify
+// segment s, thread 0 picks the winner and walks its path.
+__device__ void accept_tree(const SegArgs& sg, const int32_t* tokens, const int32_t* gv, const int32_t* parent,
+                            const int32_t* flags, int32_t* seg_accept, int32_t* result, int32_t* path,
+                            int32_t* m_sh) {
   const int s = threadIdx.x;
   if (s < sg.n) {
     int cnt = 0;
     for (int i = sg.verify_from[s]; i < sg.nrows[s]; ++i) {
       int r = sg.first[s] + i;
       int p = parent[r];
-      if (p >= 0 && tokens[r] == g[p]) ++cnt;
+      if (p >= 0 && tokens[r] == gv[p]) ++cnt;
       else break;
     }
-    m[s] = cnt;
+    m_sh[s] = cnt;
     seg_accept[s] = cnt;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    int best = 0, bm = m[0];
+    int best = 0, bm = m_sh[0];
     for (int i = 1; i < sg.n; ++i)
-      if (sg.role[i] == 1 && m[i] > bm) { best = i; bm = m[i]; }
+      if (sg.role[i] == 1 && m_sh[i] > bm) { best = i; bm = m_sh[i]; }
     int k = sg.verify_from[best] + bm;
     int last = k > 0 ? sg.first[best] + k - 1 : sg.attach[best];
     if (last < 0) last = 0;  // unreachable for validated segments (row 0 is a root)
@@ -266,9 +268,16 @@ __global__ void k_accept_tree(SegArgs sg, const int32_t* tokens, const int32_t* 
     for (int x = last; x >= 0; x = parent[x]) path[i--] = x;
     result[0] = len;
     result[1] = best;
-    result[2] = g[last];
+    result[2] = gv[last];
     result[3] = flags ? flags[0] : 0;
   }
+}
+
+__global__ void k_accept_tree(SegArgs sg, const int32_t* tokens, const int32_t* g,
+                              const int32_t* parent, int R, const int32_t* flags,
+                              int32_t* seg_accept, int32_t* result, int32_t* path) {
+  __shared__ int32_t m[16];
+  accept_tree(sg, tokens, g, parent, flags, seg_accept, result, path, m);
 }
 
 hipError_t launch_accept_tree(const SegArgs& segs, const int32_t* tokens, const int32_t* g,
@@ -277,6 +286,107 @@ hipError_t launch_accept_tree(const SegArgs& segs, const int32_t* tokens, const 
                               hipStream_t st) {
   hipLaunchKernelGGL(k_accept_tree, dim3(1), dim3(64), 0, st, segs, tokens, g, parent, R, flags,
                      seg_accept, result, path);
+  return hipGetLastError();
+}
+
+// ---- a7 tail + a8 (+ a9): argmax reduction, acceptance and commit in one launch ----
+// Block r reduces row r's per-block keys to g[r] (as k_argmax_reduce) and
+// publishes it; the last block to finish (counter state[2], re-armed by that
+// block) reads all of g and runs the step's acceptance, and for a linear
+// step asked to, its commit (C += a; the accepted rows' K/V are already in
+// place).  g travels with device-coherent (L2-bypassing) stores and loads,
+// each store complete before its block counts itself, so no L2 fence is
+// needed (the split-K hand-off of the weight-streaming GEMM, the same way).
+__device__ bool reduce_publish_last(const uint64_t* part, int nblocks, int stride, int R, int32_t* g,
+                                    int32_t* count, uint64_t* sh, int* s_last) {
+  const int r = blockIdx.x;
+  uint64_t best = 0;
+  for (int b = threadIdx.x; b < nblocks; b += blockDim.x) {
+    uint64_t k = part[(size_t)b * stride + r];
+    best = k > best ? k : best;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t other = __shfl_xor(best, o);
+    best = other > best ? other : best;
+  }
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  if (l == 0) sh[w] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) best = sh[i] > best ? sh[i] : best;
+    __hip_atomic_store(g + r, (int32_t)argmax_key_index(best), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the store is done before the count
+    const bool last = __hip_atomic_fetch_add(count, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == R - 1;
+    if (last) __hip_atomic_store(count, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *s_last = last;
+  }
+  __syncthreads();
+  return *s_last;
+}
+
+__global__ void __launch_bounds__(1024)
+    k_argmax_accept_linear(const uint64_t* part, int nblocks, int stride, const int32_t* draft, int n, int mode,
+                           uint64_t seed, int V, int32_t* state, const int32_t* flags, int32_t* result,
+                           int32_t* next_draft, int32_t* g, int commit, int max_ctx) {
+  __shared__ uint64_t sh[16];
+  __shared__ int32_t gs[kMaxRows];
+  __shared__ int s_last, s_a, s_C;
+  if (!reduce_publish_last(part, nblocks, stride, n, g, state + 2, sh, &s_last)) return;
+  const int t = threadIdx.x;
+  if (t < n) gs[t] = __hip_atomic_load(g + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (t == 0) {
+    s_a = n;
+    s_C = state[0];
+  }
+  __syncthreads();
+  if (t >= 1 && t < n && draft[t] != gs[t - 1]) atomicMin(&s_a, t);
+  __syncthreads();  // every read of draft is done (next_draft may be draft)
+  const int a = s_a, C = s_C;
+  if (t == 0) {
+    result[0] = a;
+    result[1] = 0;
+    result[2] = gs[a - 1];
+    result[3] = flags ? flags[0] : 0;
+    if (commit) state[0] = C + a > max_ctx ? max_ctx : C + a;
+  }
+  if (next_draft && t < n) {
+    const int src = a - 1 + t;
+    next_draft[t] = src < n ? gs[src] : (mode == 1 ? pad_id(seed, (int64_t)C + a + t, V) : 0);
+  }
+}
+
+__global__ void __launch_bounds__(1024)
+    k_argmax_accept_tree(const uint64_t* part, int nblocks, int stride, SegArgs sg, const int32_t* tokens, int R,
+                         const int32_t* parent, int32_t* state, const int32_t* flags, int32_t* seg_accept,
+                         int32_t* result, int32_t* path, int32_t* g) {
+  __shared__ uint64_t sh[16];
+  __shared__ int32_t gs[kMaxRows];
+  __shared__ int32_t m[16];
+  __shared__ int s_last;
+  if (!reduce_publish_last(part, nblocks, stride, R, g, state + 2, sh, &s_last)) return;
+  for (int t = threadIdx.x; t < R; t += blockDim.x) gs[t] = __hip_atomic_load(g + t, __ATOMIC_RELAXED,
+                                                                                __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  accept_tree(sg, tokens, gs, parent, flags, seg_accept, result, path, m);
+}
+
+hipError_t launch_argmax_accept_linear(const uint64_t* part, int nblocks, int stride, const int32_t* draft, int n,
+                                       int mode, uint64_t seed, int V, int32_t* state, const int32_t* flags,
+                                       int32_t* result, int32_t* next_draft, int32_t* g, int commit, int max_ctx,
+                                       hipStream_t st) {
+  if (n < 1 || n > kMaxRows || nblocks < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_argmax_accept_linear, dim3(n), dim3(1024), 0, st, part, nblocks, stride, draft, n, mode, seed,
+                     V, state, flags, result, next_draft, g, commit, max_ctx);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_accept_tree(const uint64_t* part, int nblocks, int stride, const SegArgs& segs,
+                                     const int32_t* tokens, int R, const int32_t* parent, int32_t* state,
+                                     const int32_t* flags, int32_t* seg_accept, int32_t* result, int32_t* path,
+                                     int32_t* g, hipStream_t st) {
+  if (R < 1 || R > kMaxRows || nblocks < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_argmax_accept_tree, dim3(R), dim3(1024), 0, st, part, nblocks, stride, segs, tokens, R,
+                     parent, state, flags, seg_accept, result, path, g);
   return hipGetLastError();
 }
 

@@ -21,6 +21,7 @@ JF_F32, JF_BF16 = 0, 1
 JF_ROLE_RA, JF_ROLE_CAND, JF_ROLE_PSEUDO = 0, 1, 2
 JF_MAX_SEGMENTS = 16
 JF_MAX_ROWS = 512      # rows of one step at most
+JF_STEP_COMMIT = 2     # jf_jacobi_step mode bit: commit the accepted rows in the step
 JF_VIS_WORDS = 8       # u64 words of a row's in-step visibility mask
 JF_FLAG_BAD_TOKEN, JF_FLAG_CAPACITY, JF_FLAG_SYNC = 1, 2, 4
 JF_OPT_FUSED_ATTENTION = 1

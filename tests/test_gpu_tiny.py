@@ -156,7 +156,7 @@ def test_error_paths(env):
         m.jf_jacobi_step(d, 17, 1, 0, dec.d_argmax, dec.d_result, dec.d_next)
     assert e.value.status == jf.JF_E_CAPACITY       # n > max_rows
     with pytest.raises(jf.JfError) as e:
-        m.jf_jacobi_step(d, 4, 2, 0, dec.d_argmax, dec.d_result, dec.d_next)
+        m.jf_jacobi_step(d, 4, 4, 0, dec.d_argmax, dec.d_result, dec.d_next)
     assert e.value.status == jf.JF_E_INVAL          # bad mode
     bad = [[(0, 3, -1, 0, 1), (4, 1, 0, 1, 0)],     # gap in rows
            [(0, 3, 0, 0, 1)],                       # first not a root
@@ -260,3 +260,42 @@ def test_tree_commit_moves_winning_candidate(env, m_len):
     assert ((dec.d_argmax[:n].cpu().numpy() == g2) | (gap < GAP_EXEMPT)).all()
     # and the committed tokens are the greedy continuation
     assert ar[:1 + m_len] == [tokens[r] for r in path]
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_step_commit_flag_equals_step_then_commit(env, mode):
+    """jf_jacobi_step with JF_STEP_COMMIT (argmax reduction, acceptance and
+    commit in one launch) against the step followed by jf_commit_kv: the same
+    argmax, result, next draft and committed length at every iteration of a
+    decode; no jf_commit_kv may follow a committing step."""
+    import torch
+    from paper_2512_14681_amd import decode, jf
+    V, n = SHAPE["vocab"], 8
+    runs = []
+    for fused in (False, True):
+        m = jf.Model(SHAPE, env["w"], max_rows=16, max_ctx=256)
+        dec = decode.Decoder(m)
+        p = dec.prefill(env["prompt"])
+        C = len(env["prompt"])
+        d_tok = torch.tensor([p] + [decode.pad_token(3, C + i, V) for i in range(1, n)], dtype=torch.int32,
+                             device="cuda")
+        rec = []
+        for it in range(12):
+            if fused:
+                m.jf_jacobi_step(d_tok, n, mode | jf.JF_STEP_COMMIT, 3, dec.d_argmax, dec.d_result, d_tok)
+            else:
+                m.jf_jacobi_step(d_tok, n, mode, 3, dec.d_argmax, dec.d_result, d_tok)
+                m.jf_commit_kv(None, dec.d_result)
+            rec.append((dec.d_result.cpu().numpy().copy(), dec.d_argmax[:n].cpu().numpy().copy(),
+                        d_tok.cpu().numpy().copy(), m.jf_kv_length()))
+            if mode == 0:   # block mode: restart the block from the new pending token
+                res = rec[-1][0]
+                d_tok[0] = int(res[2])
+        if fused:
+            with pytest.raises(jf.JfError) as e:
+                m.jf_commit_kv(None, dec.d_result)
+            assert e.value.status == jf.JF_E_STATE
+        runs.append(rec)
+    for (r0, g0, t0, c0), (r1, g1, t1, c1) in zip(*runs):
+        assert (r0 == r1).all() and (g0 == g1).all() and c0 == c1
+        assert (t0 == t1).all() if mode == 1 else (t0[0] == t1[0])
