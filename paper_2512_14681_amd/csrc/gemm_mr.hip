@@ -2,7 +2,7 @@
 // W[N][K]^T, for the wide Jacobi steps (more than 32 rows: multi-block
 // drafts with recycled candidates, Sec. 3.2 and App. A Alg. 1; the packed
 // training forward; the block-size sweeps): the wide projections (gate/up,
-// LM head) and the long-K narrow one (down).  Rows go in chunks of 64 or 128.
+// LM head) and the long-K narrow one (down).  Rows go in chunks of 64, 96 or 128.
 //
 // What bounds these launches is the bytes each compute unit requests (its
 // share of the weights plus the activations it re-reads), so the kernel asks
@@ -312,10 +312,13 @@ __global__ void __launch_bounds__(kRedThreads) k_mr_reduce(MrPlan m, Epi ep) {
 }
 
 // ---- plans ------------------------------------------------------------------------
-// Row tiles of a chunk: 64- and 128-row chunks (above 128 rows each chunk
-// re-reads the weights, but a wider chunk leaves registers for one column
-// tile a wave, and re-reading the activations once per 8 tiles costs more).
-int mr_row_tiles(int R) { return R <= 64 ? 4 : 8; }
+// Row tiles of a chunk: 4, 6 or 8 (64-, 96- and 128-row chunks), whichever
+// the cost below rates cheapest.  Each chunk streams the weights again, and
+// a pass re-reads the chunk's activations, so wide chunks save weight bytes
+// while narrow ones leave registers for more column tiles a wave (fewer
+// passes): 192 rows run as two 96-row chunks in one pass each rather than a
+// 128-row chunk in two passes plus a 64-row one.
+static bool mr_rt_ok(int RT) { return RT == 4 || RT == 6 || RT == 8; }
 
 // Most column tiles one pass of a group holds (groups of ceil(U / n_cg)
 // units split into `passes` parts).
@@ -329,7 +332,7 @@ static long mr_max_pass_tiles(const MrPlan& m) {
 // accumulators 4 RT B, weight ring 8 B D and activation ring 2 D RT
 // registers a lane (ring depth D = 2 half K-blocks), within the 256 of a
 // wave at two waves per SIMD (checked: no spills).
-static int mr_max_cols(int RT) { return RT == 4 ? 4 : 2; }
+static int mr_max_cols(int RT) { return RT == 4 ? 4 : RT == 6 ? 3 : 2; }
 
 // Plan cost, in compute-unit clocks: a workgroup's requested bytes (its
 // weights, the activations of its K-range once per pass at half weight, as
@@ -358,46 +361,50 @@ bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int m
   // per compute unit with a whole number of column tiles (measured: gate/up
   // 50.5 against 52.9 us, LM head 169 against 222 us at 16 rows).
   if (R <= 32 || N % 16 || K % 128) return false;
-  const int RT = mr_row_tiles(R);
-  m.R = R;
-  m.RT = RT;
-  m.KC = K / 128;
-  m.P = pack_group(N);
-  m.T = N / 16;
-  m.gr = epi_kind == EPI_SWIGLU ? 2 : 1;
-  if (m.T % m.gr) return false;
-  m.chunks = (R + 16 * RT - 1) / (16 * RT);
-  const int U = m.T / m.gr;
+  const int gr = epi_kind == EPI_SWIGLU ? 2 : 1;
+  if ((N / 16) % gr) return false;
   const int cus = std::max(1, n_cus);
-  const int per_chunk = std::max(1, cus / m.chunks);       // workgroups per row chunk in one round
-  // Measured on the 7B-shaped projections (64 and 192 rows): a matrix too
-  // narrow to give every compute unit a wave's worth of columns needs split
-  // K here, which pays (partials, a reduction launch) only over a long K
-  // (down: 64 K-blocks and more); short-K narrow matrices (QKV, O) run
-  // faster on the weight-streaming kernel's row chunks, and wide ones
-  // (gate/up, LM head) faster without split K.
-  const bool narrow = m.T < 8 * per_chunk;
-  if (narrow && m.KC < 64) return false;
-  if (!narrow) max_splits = 1;
   double best = -1;
-  MrPlan t = m;
-  for (int S = 1; S <= std::min(m.KC, std::min(max_splits, 64)); ++S) {
-    if (S > 1 && (size_t)S * R * N > kGemmPartFloats) break;
-    t.S = S;
-    t.n_cg = std::min(U, std::max(1, per_chunk / S));
-    // the fewest passes (each re-reads the activations), then the fewest
-    // tiles a wave that holds a pass (idle waves fetch nothing)
-    t.B = mr_max_cols(RT);
-    t.passes = 1;
-    while (mr_max_pass_tiles(t) > 8L * t.B) ++t.passes;
-    t.B = (int)((mr_max_pass_tiles(t) + 7) / 8);
-    const double c = mr_cost(t, cus);
-    if (best < 0 || c < best) {
-      best = c;
-      m = t;
+  for (int RT = 4; RT <= 8; RT += 2) {
+    MrPlan t{};
+    t.R = R;
+    t.RT = RT;
+    t.KC = K / 128;
+    t.P = pack_group(N);
+    t.T = N / 16;
+    t.gr = gr;
+    t.chunks = (R + 16 * RT - 1) / (16 * RT);
+    const int U = t.T / t.gr;
+    const int per_chunk = std::max(1, cus / t.chunks);     // workgroups per row chunk in one round
+    // Measured on the 7B-shaped projections (64 and 192 rows): a matrix too
+    // narrow to give every compute unit a wave's worth of columns needs
+    // split K here, which pays (partials, a reduction launch) only over a
+    // long K (down: 64 K-blocks and more); short-K narrow matrices (QKV, O)
+    // run faster on the weight-streaming kernel's row chunks, and wide ones
+    // (gate/up, LM head) faster without split K.
+    // (judged at the widest chunk, so that the choice of chunk does not
+    // move a matrix between kernels)
+    const bool narrow = t.T < 8 * std::max(1, cus / ((R + 127) / 128));
+    if (narrow && t.KC < 64) return false;
+    const int splits = narrow ? max_splits : 1;
+    for (int S = 1; S <= std::min(t.KC, std::min(splits, 64)); ++S) {
+      if (S > 1 && (size_t)S * R * N > kGemmPartFloats) break;
+      t.S = S;
+      t.n_cg = std::min(U, std::max(1, per_chunk / S));
+      // the fewest passes (each re-reads the activations), then the fewest
+      // tiles a wave that holds a pass (idle waves fetch nothing)
+      t.B = mr_max_cols(RT);
+      t.passes = 1;
+      while (mr_max_pass_tiles(t) > 8L * t.B) ++t.passes;
+      t.B = (int)((mr_max_pass_tiles(t) + 7) / 8);
+      const double c = mr_cost(t, cus);
+      if (best < 0 || c < best) {
+        best = c;
+        m = t;
+      }
     }
   }
-  return true;
+  return best >= 0;
 }
 
 size_t gemm_mr_lds_bytes(const MrPlan& m) {
@@ -425,7 +432,7 @@ static hipError_t launch_mr_b(const void* X, size_t xplane, const void* Wp, cons
   switch (m.B) {
     case 1: return launch_mr_t<RT, 1>(X, xplane, Wp, m, ep, st);
     case 2: return launch_mr_t<RT, 2>(X, xplane, Wp, m, ep, st);
-    case 3: if constexpr (RT == 4) return launch_mr_t<RT, 3>(X, xplane, Wp, m, ep, st); break;
+    case 3: if constexpr (RT <= 6) return launch_mr_t<RT, 3>(X, xplane, Wp, m, ep, st); break;
     case 4: if constexpr (RT == 4) return launch_mr_t<RT, 4>(X, xplane, Wp, m, ep, st); break;
     default: break;
   }
@@ -439,7 +446,7 @@ int gemm_mr_part_blocks(const MrPlan& m) {
 hipError_t launch_gemm_mr(const void* X, size_t xplane, const void* Wp, const MrPlan& m, const Epi& ep,
                           hipStream_t st) {
   if (m.R < 1 || m.T < 1 || m.KC < 1 || m.n_cg < 1 || m.S < 1 || m.S > m.KC || m.passes < 1 || m.gr < 1 || m.B < 1 ||
-      m.RT != mr_row_tiles(m.R) || m.B > mr_max_cols(m.RT) || m.T % m.gr ||
+      !mr_rt_ok(m.RT) || m.B > mr_max_cols(m.RT) || m.T % m.gr ||
       m.chunks != (m.R + 16 * m.RT - 1) / (16 * m.RT) || ep.row0 != 0)
     return hipErrorInvalidValue;
   // every pass must fit the waves' column tiles (8 waves of at most B)
@@ -448,6 +455,7 @@ hipError_t launch_gemm_mr(const void* X, size_t xplane, const void* Wp, const Mr
   if (m.S > 1 && (!ep.kpart || (size_t)m.S * m.R * m.T * 16 > kGemmPartFloats)) return hipErrorInvalidValue;
   switch (m.RT) {
     case 4: return launch_mr_b<4>(X, xplane, Wp, m, ep, st);
+    case 6: return launch_mr_b<6>(X, xplane, Wp, m, ep, st);
     case 8: return launch_mr_b<8>(X, xplane, Wp, m, ep, st);
     default: return hipErrorInvalidValue;
   }

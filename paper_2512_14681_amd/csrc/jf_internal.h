@@ -102,7 +102,7 @@ size_t gemm_blocks(const GemmShape& s);
 // kernel reduces.
 struct MrPlan {
   int R;            // rows
-  int RT;           // row tiles per chunk (4, 8): 16 RT rows per chunk
+  int RT;           // row tiles per chunk (4, 6, 8): 16 RT rows per chunk
   int B;            // column tiles per wave at most
   int KC;           // 128-wide K-blocks
   int P;            // pack group of the weight matrix
@@ -113,7 +113,6 @@ struct MrPlan {
   int S;            // K splits (partials in Epi::kpart, S x R x N floats)
   int chunks;       // row chunks of 16 RT rows
 };
-int mr_row_tiles(int R);
 // false if the shape is not for this kernel; max_splits 1: no split-K
 // scratch
 bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int max_splits);

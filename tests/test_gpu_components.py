@@ -116,6 +116,21 @@ def test_lm_head_acceptance_closed_form():
     assert res[0] == R
 
 
+@pytest.mark.parametrize("R", [48, 80, 96, 144, 192])
+def test_lm_head_column_slice_chunks(R):
+    """A vocabulary wide enough for the column-slice GEMM (2048 tiles of 16
+    columns, K = 1024): 64-, 96- and 128-row chunks, one or two of them,
+    with ragged last chunks (80 = 96 - 16, 144 = 96 + 48).  bf16 values,
+    plain fp64 product and argmax."""
+    d, V = 1024, 32768
+    x = jf_inputs.normal(5, 1, R * d, dtype="bf16").reshape(R, d)
+    w = jf_inputs.normal(5, 2, V * d, std=0.02, dtype="bf16").reshape(V, d)
+    z = bf16_bits_to_float(x) @ bf16_bits_to_float(w).T
+    g, _, logits = run_lm_head(x, w, R, d, V, "bf16")
+    assert np.abs(logits - z).max() < 1e-3
+    assert ((g == np.argmax(z, axis=1)) | (top2(z) < 1e-3)).all()
+
+
 def test_lm_head_full_size_config3():
     """LM head of the 7B shape: hidden [64, 3584] ~ N(0,1), W [152064, 3584] ~
     N(0, 0.02), bf16; per-row argmax and the perturbed-draft acceptance."""
