@@ -376,16 +376,19 @@ bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int m
     t.chunks = (R + 16 * RT - 1) / (16 * RT);
     const int U = t.T / t.gr;
     const int per_chunk = std::max(1, cus / t.chunks);     // workgroups per row chunk in one round
-    // Measured on the 7B-shaped projections (64 and 192 rows): a matrix too
+    // Measured on the 7B-shaped projections (64 to 256 rows): a matrix too
     // narrow to give every compute unit a wave's worth of columns needs
-    // split K here, which pays (partials, a reduction launch) only over a
-    // long K (down: 64 K-blocks and more); short-K narrow matrices (QKV, O)
-    // run faster on the weight-streaming kernel's row chunks, and wide ones
-    // (gate/up, LM head) faster without split K.
-    // (judged at the widest chunk, so that the choice of chunk does not
-    // move a matrix between kernels)
+    // split K here, which pays (partials, a reduction launch) over a long K
+    // (down: 64 K-blocks and more) at any row count, and over a short K
+    // (QKV, O) from 96 rows, where the weight-streaming kernel's 32-row
+    // chunks stream the weights three times or more (steps at 96 / 192 /
+    // 256 rows: -3.4 / -2.7 / -7.2%; at 64 rows QKV 23.6 -> 25.4 us, O
+    // 16.1 -> 25.6 us, so below 96 rows they stay there); wide matrices
+    // (gate/up, LM head) run faster without split K.  Narrowness is judged
+    // at the widest chunk, so that the choice of chunk does not move a
+    // matrix between kernels.
     const bool narrow = t.T < 8 * std::max(1, cus / ((R + 127) / 128));
-    if (narrow && t.KC < 64) return false;
+    if (narrow && t.KC < 64 && R < 96) return false;
     const int splits = narrow ? max_splits : 1;
     for (int S = 1; S <= std::min(t.KC, std::min(splits, 64)); ++S) {
       if (S > 1 && (size_t)S * R * N > kGemmPartFloats) break;
