@@ -42,18 +42,32 @@ template <typename T, int RT, int NT, int WK> struct Ring {
 // CHUNKED (C > 1): the 1-D XCD-aware block order above, and the weights,
 // read by the C chunk blocks of a unit, are loaded with the ordinary
 // (L2-allocating) policy instead of the streaming hint.  Otherwise the grid
-// is (column groups, K splits) and there is one chunk.
+// is (column groups, K splits) and there is one chunk, or, with a tail split
+// (full < groups), 1-D: blocks [0, full) take column groups [0, full) whole
+// and the remaining groups take S blocks each, one K-range apiece.
 template <typename T, int RT, int NT, int WK, int D = Ring<T, RT, NT, WK>::D, bool CHUNKED = false>
 __global__ void __launch_bounds__(64 * WK)
 k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC, int P, int groups,
-       int S, int C, Epi ep) {
+       int S, int C, int full, Epi ep) {
   extern __shared__ float lds[];
   constexpr bool PX = Ring<T, RT, NT, WK>::kPrefetchX;
   constexpr int RX = PX ? RT : 1;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   int z = 0, ng = blockIdx.x, ks = blockIdx.y;
-  if constexpr (CHUNKED) {
+  int Sb = S;                                      // K splits of this block's column group
+  if constexpr (!CHUNKED) {
+    if (full < groups) {
+      const int b = blockIdx.x;
+      if (b < full) {
+        ks = 0;
+        Sb = 1;
+      } else {
+        ng = full + (b - full) / S;
+        ks = (b - full) % S;
+      }
+    }
+  } else {
     const int b = blockIdx.x;
     z = (b >> 3) % C;                              // row chunk
     const int u = ((b >> 3) / C) * 8 + (b & 7);    // unit: column group + K split
@@ -65,7 +79,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
   const int rb = CR * z;                           // the chunk's first output row
   const int Rs = CHUNKED ? CR : ep.R;              // rows per chunk (partial-tile stride)
   const int R = CHUNKED ? min(CR, ep.R - rb) : ep.R;  // rows of this chunk
-  const int kb0 = (KC * ks) / S, kb1 = (KC * (ks + 1)) / S;   // this block's K-blocks
+  const int kb0 = (KC * ks) / Sb, kb1 = (KC * (ks + 1)) / Sb;  // this block's K-blocks
   const int kc0 = kb0 + ((kb1 - kb0) * wave) / WK;
   const int kc1 = kb0 + ((kb1 - kb0) * (wave + 1)) / WK;
   const int nk = kc1 - kc0;
@@ -195,7 +209,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     }
   }
   __syncthreads();
-  if (S > 1) {
+  if (Sb > 1) {
     // Split-K over blocks: publish this block's partial tile; the block that
     // arrives last for this column group sums all partials in split order
     // (deterministic) and runs the epilogue, then re-arms the counter.
@@ -209,7 +223,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     // split saves; the wait below is the one ordering the stores need.
     __shared__ int s_last;
     const int cols = NT * 16;
-    const size_t unit_part = ((size_t)ng * C + z) * S;  // this chunk's S partial tiles
+    const size_t unit_part = ((size_t)ng * C + z) * Sb;  // this chunk's Sb partial tiles
     float* mine = ep.kpart + (unit_part + ks) * (size_t)(Rs * cols);
     for (int e = threadIdx.x; e < R * cols; e += 64 * WK) {
       const int row = e / cols, c = e - row * cols;
@@ -218,7 +232,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stores are done
     __syncthreads();
     if (threadIdx.x == 0)
-      s_last = __hip_atomic_fetch_add(ep.kcount + ng * C + z, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+      s_last = __hip_atomic_fetch_add(ep.kcount + ng * C + z, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == Sb - 1;
     __syncthreads();
     if (!s_last) return;
     // Loads are issued four splits at a time so that their latencies
@@ -228,7 +242,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     for (int e = threadIdx.x; e < R * cols; e += 64 * WK) {
       float sum = 0.f;
       int k = 0;
-      for (; k + 4 <= S; k += 4) {
+      for (; k + 4 <= Sb; k += 4) {
         float v[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -236,7 +250,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
 #pragma unroll
         for (int i = 0; i < 4; ++i) sum += v[i];
       }
-      for (; k < S; ++k)
+      for (; k < Sb; ++k)
         sum += __hip_atomic_load(all + k * pstride + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const int row = e / cols, c = e - row * cols;
       tile[row * tld + c] = sum;
@@ -400,6 +414,28 @@ void gemm_plan(GemmShape& s, int epi_kind) {
 
 size_t gemm_blocks(const GemmShape& s) { return (size_t)s.N / (16 * s.NT); }
 
+// A launch of G whole-K workgroups on n compute units runs floor(G / n)
+// even rounds and a last one that leaves most units idle, while the time is
+// set by the units with the most weight bytes to stream (the rate each unit
+// sustains is the bound).  Splitting only the last round's groups over K
+// into S = n / (G mod n) blocks evens the units out: gate/up at 16 rows
+// (592 groups) gives 80 units 3 groups and the rest 2; split, every unit
+// streams at most 2 1/3 (48.1 against 50.7 us).  Only where the last round
+// costs 15% or more: the partials and the last block's reduction at the
+// end of the launch cost more than the LM head's 8% (2376 groups, 9.28
+// rounds: 169 -> 172 us split).
+void gemm_tail_split(GemmShape& s, int n_cus) {
+  const int groups = s.N / (16 * s.NT);
+  const int KC = s.K / 128;
+  if (s.C != 1 || s.S != 1 || n_cus < 1 || groups <= n_cus) return;
+  const int rem = groups % n_cus;
+  if (rem == 0 || (double)(groups / n_cus + 1) * n_cus < 1.15 * groups) return;
+  const int S = std::min(n_cus / rem, KC / s.WK);
+  if (S < 2 || (size_t)s.N * S * s.R > kGemmPartFloats || (size_t)groups > kGemmCounters) return;
+  s.full = groups - rem;
+  s.S = S;
+}
+
 static unsigned grid_blocks(const GemmShape& s) {
   const int units = s.N / (16 * s.NT) * s.S;
   return (unsigned)((units + 7) / 8 * 8 * s.C);
@@ -413,11 +449,15 @@ static hipError_t launch_t(const void* X, size_t xplane, const void* Wp, const G
   if (s.C > 1)
     hipLaunchKernelGGL((k_gemm<T, RT, NT, WK, D, true>), dim3(grid_blocks(s)), dim3(64 * WK), lds, st,
                        reinterpret_cast<const T*>(X), xplane, reinterpret_cast<const T*>(Wp), s.K / 128,
-                       pack_group(s.N), groups, s.S, s.C, ep);
+                       pack_group(s.N), groups, s.S, s.C, groups, ep);
+  else if (s.full > 0)
+    hipLaunchKernelGGL((k_gemm<T, RT, NT, WK, D, false>), dim3(s.full + (groups - s.full) * s.S), dim3(64 * WK),
+                       lds, st, reinterpret_cast<const T*>(X), xplane, reinterpret_cast<const T*>(Wp), s.K / 128,
+                       pack_group(s.N), groups, s.S, 1, s.full, ep);
   else
     hipLaunchKernelGGL((k_gemm<T, RT, NT, WK, D, false>), dim3(groups, s.S), dim3(64 * WK), lds, st,
                        reinterpret_cast<const T*>(X), xplane, reinterpret_cast<const T*>(Wp), s.K / 128,
-                       pack_group(s.N), groups, s.S, 1, ep);
+                       pack_group(s.N), groups, s.S, 1, groups, ep);
   return hipGetLastError();
 }
 
@@ -468,6 +508,8 @@ hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
     return hipErrorInvalidValue;
   if (s.C != (s.R > kChunkRows ? (s.R + kChunkRows - 1) / kChunkRows : 1)) return hipErrorInvalidValue;
   if (s.S < 1 || s.S > s.K / 128) return hipErrorInvalidValue;
+  if (s.full < 0 || (s.full > 0 && (s.C != 1 || s.S < 2 || s.full >= s.N / (16 * s.NT))))
+    return hipErrorInvalidValue;
   const size_t rows = s.C > 1 ? (size_t)kChunkRows * s.C : (size_t)s.R;
   if (s.S > 1 && (!ep.kpart || !ep.kcount || (size_t)(s.N / (16 * s.NT)) * s.C > kGemmCounters ||
                   (size_t)s.N * s.S * rows > kGemmPartFloats))

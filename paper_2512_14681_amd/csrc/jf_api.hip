@@ -401,6 +401,7 @@ static hipError_t run_gemm(int dtype, int R, int N, int K, const void* X, size_t
   GemmShape gs{R, N, K, 1, 1, 1};
   gemm_plan(gs, ep.kind);
   if (!split_k) gs.S = 1;
+  else gemm_tail_split(gs, device_cus());
   if (part_blocks) *part_blocks = (int)gemm_blocks(gs);
   return launch_gemm(dtype, X, xplane, W, gs, ep, st);
 }

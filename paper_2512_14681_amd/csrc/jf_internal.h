@@ -81,6 +81,8 @@ struct GemmShape {
   int S;         // blocks splitting K per column group
   int D;         // register-ring depth (0: the kernel's default)
   int C;         // row chunks of at most 32 rows (blocks per column group and split)
+  int full;      // tail split (C = 1, 0 < full < groups): column groups [0, full)
+                 // run whole, the remaining ones split K over S blocks; 0: off
 };
 
 // Scratch a GEMM needs for split-K partials (floats) and counters (ints).
@@ -90,6 +92,10 @@ constexpr size_t kGemmCounters = 16384;
 // Chooses NT / WK / S / C for a shape (NT fixed by the epilogue where it
 // matters).
 void gemm_plan(GemmShape& s, int epi_kind);
+// Balances the last, partial round of a plan's workgroups over n_cus
+// compute units by splitting its column groups over K (sets full and S);
+// needs split-K scratch.
+void gemm_tail_split(GemmShape& s, int n_cus);
 // X: activation planes of an [R][K] matrix in the GEMM-input layout
 // (act_offset; planes xplane elements apart for bf16 models).
 hipError_t launch_gemm(int dtype, const void* X, size_t xplane, const void* Wp,
