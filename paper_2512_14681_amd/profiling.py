@@ -165,8 +165,9 @@ def _step_phases(rows, layers):
     by phase, from the launch order of one forward: k_embed, then per layer
     the QKV projection, attention (+ its split merge), the O projection, the
     gate/up and the down projection, then the LM head and its tail.  A
-    forward is kept when it ends in an acceptance kernel (a step, not a
-    prefill chunk).  Returns {phase: [values]}."""
+    forward is kept when it ends in an acceptance kernel (k_accept_*, or the
+    fused k_argmax_accept_*: a step, not a prefill chunk).  Returns {phase:
+    [values]}."""
     forwards, cur = [], None
     for did, name, v in rows:
         n = short_name(name)
@@ -178,7 +179,7 @@ def _step_phases(rows, layers):
     gemm_phase = ("qkv", "o", "gateup", "down")
     out = {}
     for f in forwards:
-        if not any(n.startswith("k_accept") for n, _ in f):
+        if not any(n.startswith(("k_accept", "k_argmax_accept")) for n, _ in f):
             continue
         gi = 0
         for n, v in f:
