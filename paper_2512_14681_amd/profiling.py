@@ -17,7 +17,7 @@
         GRBM_GUI_ACTIVE (one pass): issued bf16 flops, the matrix cores' busy
         fraction, and the algorithmic flops of R rows at committed length C;
         forwards are kept when one of their kernels matches REGEX
-        (k_accept: the Jacobi steps; k_tree_packed: the packed forward).
+        (default accept: the Jacobi steps; k_tree_packed: the packed forward).
 
     python -m paper_2512_14681_amd.profiling ceiling [--gib G] [--reps K]
         HBM rates that plain library kernels reach on the device (GPU
@@ -257,7 +257,8 @@ def _label_forward(f, layers):
             lab = "lm_head" if gi == 4 * layers else gemm_phase[gi % 4]
             gi += 1
         elif n.startswith("k_mr_reduce"):
-            lab = "down_reduce" if gi % 4 == 0 and gi > 0 else "reduce"
+            # the split-K reduction of the projection launched just before
+            lab = ("lm_head" if gi == 4 * layers + 1 else gemm_phase[(gi - 1) % 4]) + "_reduce" if gi > 0 else "reduce"
         elif n.startswith("k_attn_combine"):
             lab = "attn_combine"
         elif n.startswith("k_attn"):
@@ -291,7 +292,8 @@ def step_mfma(directory, select, rows, ctx, layers=28, clock_ghz=2.4, simds=1024
              "| phase | dispatches | us (counter run) | issued bf16 GFLOP | algorithmic GFLOP | issued / algorithmic "
              "| issued TFLOP/s | MFMA busy |",
              "|---|---:|---:|---:|---:|---:|---:|---:|"]
-    order = ["qkv", "attn", "attn_combine", "o", "gateup", "down", "down_reduce", "lm_head"]
+    order = ["qkv", "qkv_reduce", "attn", "attn_combine", "o", "o_reduce", "gateup", "down", "down_reduce",
+             "lm_head"]
     tot = {"ns": 0.0, "mops": 0.0, "algo": 0.0, "busy": 0.0, "grbm": 0.0}
     for lab in order + sorted(k for k in per if k not in order):
         if lab not in per:
@@ -421,7 +423,8 @@ def main(argv=None):
     stt.add_argument("--ctx", type=int, default=1024, help="committed length (for the attention bytes)")
     sm = sub.add_parser("step-mfma", help="MFMA load of every phase of the forwards in a --pmc run")
     sm.add_argument("dir")
-    sm.add_argument("--select", default="k_accept", help="regex: keep forwards with a matching kernel")
+    sm.add_argument("--select", default="accept", help="regex: keep forwards with a matching kernel "
+                    "(default: the steps, which end in an acceptance kernel)")
     sm.add_argument("--rows", type=int, required=True)
     sm.add_argument("--ctx", type=int, required=True, help="committed length the forwards attend over")
     c = sub.add_parser("ceiling")
