@@ -93,6 +93,12 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
   if (ep.ss_clear && ng == 0 && ks == 0 && z == 0)
     for (int i = threadIdx.x; i < 3 * ep.ss_stride; i += blockDim.x)
       __hip_atomic_store(ep.ss_clear + i, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // the residual-add epilogue's operands that do not depend on the product,
+  // loaded now for the same reason; the 4-tile kernels with a 2-deep ring
+  // have no registers to spare for them
+  constexpr bool kPre = !(NT == 4 && D >= 2);
+  EpiPre pre;
+  if constexpr (kPre) epilogue_prefetch(pre, NT * 16, ng * NT * 16, ep, threadIdx.x, blockDim.x, rb, R);
 
   f32x4_t acc[RT][NT];
 #pragma unroll
@@ -279,7 +285,7 @@ k_gemm(const T* __restrict__ X, size_t xplane, const T* __restrict__ Wp, int KC,
     }
     __syncthreads();
   }
-  epilogue<T>(tile, tld, NT * 16, ng * NT * 16, ep, ng, threadIdx.x, blockDim.x, rb, R);
+  epilogue<T>(tile, tld, NT * 16, ng * NT * 16, ep, ng, threadIdx.x, blockDim.x, rb, R, kPre ? &pre : nullptr);
 }
 
 // Rows per chunk of a GEMM with more rows than that: 32 (2 row tiles per
