@@ -19,6 +19,12 @@
         forwards are kept when one of their kernels matches REGEX
         (default accept: the Jacobi steps; k_tree_packed: the packed forward).
 
+    python -m paper_2512_14681_amd.profiling attn-traffic --fetch DIR1 --write DIR2 --copy-bytes N
+        HBM bytes per call of the attention workload (``bench.py --only
+        attention --copy-probe``: 9 shapes P x n, 68 calls each, each call the
+        attention kernel and, when it splits the keys, its merge), per shape,
+        against the shape's algorithmic bytes.
+
     python -m paper_2512_14681_amd.profiling ceiling [--gib G] [--reps K]
         HBM rates that plain library kernels reach on the device (GPU
         required): a full read of a G GiB bf16 tensor (torch's sum, fp32
@@ -224,6 +230,50 @@ def step_traffic(fetch_dir, write_dir, copy_bytes, layers=28, algo=None):
     return "\n".join(lines)
 
 
+ATTN_SHAPES = [(P, n) for P in (512, 2048, 8192) for n in (16, 32, 64)]  # bench.py's order
+
+
+def attn_traffic(fetch_dir, write_dir, copy_bytes, shapes=None, calls=68, H=28, G=4, hd=128):
+    """HBM bytes per call of each shape of the attention workload: the
+    dispatches of the attention kernels in order, a call being one attention
+    launch (k_attn / k_attn_lds) plus its merge (k_attn_combine) if any,
+    `calls` calls a shape; FETCH_SIZE and WRITE_SIZE scaled by the copy
+    probe as in traffic().  Algorithmic bytes: K and V of the P + n keys, q
+    in and the output out at bf16 (the workload's own figure)."""
+    shapes = shapes or ATTN_SHAPES
+    per = {}
+    for label, directory, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = _per_dispatch(directory, counter)
+        copies = [v for _, k, v in rows if "copy" in k.lower()][:3]
+        if len(copies) < 3:
+            raise RuntimeError(f"{counter}: fewer than 3 copy dispatches in {directory}")
+        scale = copy_bytes / (sum(copies) / 3 * 1024)
+        main = -1
+        for _, name, v in rows:
+            n = short_name(name)
+            if not n.startswith("k_attn"):
+                continue
+            if not n.startswith("k_attn_combine"):
+                main += 1
+            si = main // calls
+            if si < 0 or si >= len(shapes):
+                continue
+            d = per.setdefault(si, {"fetch": 0.0, "write": 0.0, "kernels": set()})
+            d[label] += v * 1024 * scale
+            d["kernels"].add(re.sub(r"<.*", "", n))
+    lines = ["| P | n | kernels | FETCH bytes per call | WRITE bytes per call | HBM bytes per call "
+             "| algorithmic bytes | ratio |", "|---:|---:|---|---:|---:|---:|---:|---:|"]
+    for si, (P, n) in enumerate(shapes):
+        if si not in per:
+            continue
+        d = per[si]
+        fb, wb = d["fetch"] / calls, d["write"] / calls
+        algo = (P + n) * G * hd * 2 * 2 + n * H * hd * 2 + n * H * hd * 4
+        lines.append(f"| {P} | {n} | {', '.join(sorted(d['kernels']))} | {fb:,.0f} | {wb:,.0f} | {fb + wb:,.0f} | "
+                     f"{algo:,} | {(fb + wb) / algo:.2f} |")
+    return "\n".join(lines)
+
+
 MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
 
 
@@ -421,6 +471,11 @@ def main(argv=None):
     stt.add_argument("--layers", type=int, default=28)
     stt.add_argument("--n", type=int, default=16, help="rows of the steps (for the algorithmic bytes)")
     stt.add_argument("--ctx", type=int, default=1024, help="committed length (for the attention bytes)")
+    at = sub.add_parser("attn-traffic", help="HBM bytes per call of each attention workload shape")
+    at.add_argument("--fetch", required=True)
+    at.add_argument("--write", required=True)
+    at.add_argument("--copy-bytes", type=int, required=True)
+    at.add_argument("--calls", type=int, default=68, help="calls per shape (bench.py: 4 warm-up + 64 timed)")
     sm = sub.add_parser("step-mfma", help="MFMA load of every phase of the forwards in a --pmc run")
     sm.add_argument("dir")
     sm.add_argument("--select", default="accept", help="regex: keep forwards with a matching kernel "
@@ -440,6 +495,8 @@ def main(argv=None):
         print(ceiling(a.gib, a.reps), flush=True)
     elif a.cmd == "step-mfma":
         print(step_mfma(a.dir, a.select, a.rows, a.ctx))
+    elif a.cmd == "attn-traffic":
+        print(attn_traffic(a.fetch, a.write, a.copy_bytes, calls=a.calls))
     elif a.cmd == "step-traffic":
         print(step_traffic(a.fetch, a.write, a.copy_bytes, a.layers, algo_bytes_7b(a.n, a.ctx)))
     elif a.cmd == "stats":

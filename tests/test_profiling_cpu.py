@@ -50,3 +50,30 @@ def test_step_mfma_labels_and_fractions(tmp_path):
     # busy: 1024 SIMDs x 100 cycles over 400 active cycles an XCD (8 XCDs summed)
     assert "| qkv | 2 | 2.0 |" in out
     assert out.count("| 0.250 |") >= 6
+
+
+def write_counter(path, counter, named_values):
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "x_counter_collection.csv"), "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(COLS)
+        for i, (n, v) in enumerate(named_values):
+            w.writerow([i, i, "Agent 1", 1, 1, 1, 512, 1, n, 256, 0, 0, 64, 0, 32, counter, v, 0, 1000])
+
+
+def test_attn_traffic_splits_calls_by_shape(tmp_path):
+    """Two shapes of two calls: the first runs the split kernel and its merge,
+    the second the LDS-shared kernel alone; counters scale by the copy probe
+    (FETCH_SIZE reads half a copy's bytes here: 1 KiB counted per 2 KiB)."""
+    copy = [("__amd_rocclr_copyBuffer", 2.0)] * 3               # 2 KiB counted per 4 KiB copied
+    calls = [("void jf::k_attn<unsigned short, 128, 1>(jf::AttnArgs)", 10.0),
+             ("void jf::k_attn_combine<unsigned short, 128, 8>(jf::AttnArgs)", 2.0)] * 2 + \
+            [("jf::k_attn_lds(jf::AttnArgs)", 6.0)] * 2
+    write_counter(str(tmp_path / "f"), "FETCH_SIZE", copy + calls)
+    write_counter(str(tmp_path / "w"), "WRITE_SIZE", copy + [(n, 1.0) for n, _ in calls])
+    out = profiling.attn_traffic(str(tmp_path / "f"), str(tmp_path / "w"), 4096, shapes=[(512, 16), (512, 32)],
+                                 calls=2)
+    lines = out.splitlines()
+    # scale 4096 / 2048 = 2: shape 1 fetches (10 + 2) KiB x 2 per call, writes 2 KiB x 2
+    assert lines[2].startswith("| 512 | 16 | k_attn, k_attn_combine | 24,576 | 4,096 | 28,672 |")
+    assert lines[3].startswith("| 512 | 32 | k_attn_lds | 12,288 | 2,048 | 14,336 |")
