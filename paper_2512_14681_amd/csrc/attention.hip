@@ -615,14 +615,18 @@ __global__ void __launch_bounds__(512, 1) k_attn_lds(AttnArgs a) {
 constexpr long kAttnQt2Work = 50000;
 
 // The LDS-shared form: query groups of up to 8 tiles (balanced), and key
-// splits of at least one page up to about 256 blocks in all.
+// splits of at least 3 pages up to about 256 blocks in all.  Splits of one
+// or two pages cost more in partials and their merge than the extra blocks
+// gain inside a step (1024-token prefix: 64 rows 5182 -> 5066 us, 128 rows
+// 7171 -> 6943 us; 192 and 256 rows unchanged; the attention workload at
+// P = 2048 / n = 64 21.7 -> 21.2 us, at P = 512 / n = 64 15.6 -> 16.6 us).
 static void attn_lds_plan(AttnArgs& a) {
   const int ntiles = ((a.H / a.G) * a.R + 15) / 16;
   const int groups = (ntiles + 7) / 8;
   a.qg = (ntiles + groups - 1) / groups;
   const int pages = (a.keys_ub + kPage - 1) / kPage;
   int s = (256 + a.G * groups - 1) / (a.G * groups);
-  s = std::min(s, pages);
+  s = std::min(s, (pages + 2) / 3);
   const int min_s = (pages + kAttnMaxPages - 3) / (kAttnMaxPages - 2);
   a.splits = std::max(1, std::min(kAttnMaxSplits, std::max(s, min_s)));
 }
