@@ -389,7 +389,12 @@ bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int m
     // matrix between kernels.
     const bool narrow = t.T < 8 * std::max(1, cus / ((R + 127) / 128));
     if (narrow && t.KC < 64 && R < 96) return false;
-    const int splits = narrow ? max_splits : 1;
+    // at most 8 K splits: the cost below rates more splits cheaper than they
+    // run (1024-token prefix, steps at 48 / 64 / 96 / 128 / 192 / 256 rows,
+    // down with 17 / 17 / 17 / 17 / 9 / 9 splits and O with 10 at 96 rows ->
+    // at most 8: -2.7 / -2.8 / -3.1 / -1.4 / -5.4 / -2.9%; capped at 6 or 4:
+    // slower again)
+    const int splits = narrow ? std::min(max_splits, 8) : 1;
     for (int S = 1; S <= std::min(t.KC, std::min(splits, 64)); ++S) {
       if (S > 1 && (size_t)S * R * N > kGemmPartFloats) break;
       t.S = S;
