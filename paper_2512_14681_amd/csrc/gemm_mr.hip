@@ -380,15 +380,15 @@ bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int m
     // narrow to give every compute unit a wave's worth of columns needs
     // split K here, which pays (partials, a reduction launch) over a long K
     // (down: 64 K-blocks and more) at any row count, and over a short K
-    // (QKV, O) from 96 rows, where the weight-streaming kernel's 32-row
-    // chunks stream the weights three times or more (steps at 96 / 192 /
-    // 256 rows: -3.4 / -2.7 / -7.2%; at 64 rows QKV 23.6 -> 25.4 us, O
-    // 16.1 -> 25.6 us, so below 96 rows they stay there); wide matrices
+    // (QKV, O) from 65 rows, where the weight-streaming kernel's 32-row
+    // chunks stream the weights three times or more (steps at 80 / 96 /
+    // 192 / 256 rows: -4.6 / -3.4 / -2.7 / -7.2%; at 33 / 48 / 64 rows
+    // +1.7 / +2.5 / +1.4%, so up to 64 rows they stay there); wide matrices
     // (gate/up, LM head) run faster without split K.  Narrowness is judged
     // at the widest chunk, so that the choice of chunk does not move a
     // matrix between kernels.
     const bool narrow = t.T < 8 * std::max(1, cus / ((R + 127) / 128));
-    if (narrow && t.KC < 64 && R < 96) return false;
+    if (narrow && t.KC < 64 && R <= 64) return false;
     // at most 8 K splits: the cost below rates more splits cheaper than they
     // run (1024-token prefix, steps at 48 / 64 / 96 / 128 / 192 / 256 rows,
     // down with 17 / 17 / 17 / 17 / 9 / 9 splits and O with 10 at 96 rows ->

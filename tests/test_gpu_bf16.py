@@ -69,6 +69,29 @@ def test_step_logits(env):
     assert ok.all()
 
 
+@pytest.mark.parametrize("n", [80, 96])
+def test_step_logits_column_slice_rows(env, n):
+    """Steps of 65 to 96 rows run every projection on the column-slice GEMM
+    (QKV and O with split K and the ordered reduction): all rows' logits
+    against the teacher-forced oracle."""
+    import torch
+    from paper_2512_14681_amd import decode, jf
+    model = jf.Model(SHAPE, env["w"], max_rows=96, max_ctx=512)
+    dec = decode.Decoder(model)
+    p = dec.prefill(env["prompt"])
+    draft = [p] + [ojac.pad_id(4, 80 + i, SHAPE["vocab"]) for i in range(1, n)]
+    d_draft = torch.tensor(draft, dtype=torch.int32, device="cuda")
+    d_next = torch.zeros(n, dtype=torch.int32, device="cuda")
+    d_log = torch.empty((n, SHAPE["vocab"]), dtype=torch.float32, device="cuda")
+    model.jf_jacobi_step(d_draft, n, 1, 4, dec.d_argmax, dec.d_result, d_next, d_log)
+    z = d_log.cpu().numpy()
+    g = dec.d_argmax[:n].cpu().numpy()
+    zo = teacher_forced(env, list(env["prompt"]) + draft)[80:80 + n]
+    err = np.abs(z - zo).max()
+    assert err < LOGIT_TOL, err
+    assert ((g == zo.argmax(1)) | (gaps(zo) < GAP_EXEMPT)).all()
+
+
 @pytest.mark.parametrize("n,mode", [(16, "window"), (8, "block")])
 def test_decode_matches_oracle_argmax(env, n, mode):
     dec = env["dec"]
