@@ -1,8 +1,9 @@
 // Column-slice GEMM of the decoder's projections, Y[R][N] = X[R][K] *
-// W[N][K]^T, for the wide Jacobi steps (more than 32 rows: multi-block
+// W[N][K]^T, for the wide Jacobi steps (more than 24 rows: multi-block
 // drafts with recycled candidates, Sec. 3.2 and App. A Alg. 1; the packed
 // training forward; the block-size sweeps): the wide projections (gate/up,
-// LM head) and the long-K narrow one (down).  Rows go in chunks of 64, 96 or 128.
+// LM head) and the long-K narrow one (down), and from 65 rows QKV and O.
+// Rows go in chunks of 32, 64, 96 or 128.
 //
 // What bounds these launches is the bytes each compute unit requests (its
 // share of the weights plus the activations it re-reads), so the kernel asks
@@ -312,13 +313,13 @@ __global__ void __launch_bounds__(kRedThreads) k_mr_reduce(MrPlan m, Epi ep) {
 }
 
 // ---- plans ------------------------------------------------------------------------
-// Row tiles of a chunk: 4, 6 or 8 (64-, 96- and 128-row chunks), whichever
-// the cost below rates cheapest.  Each chunk streams the weights again, and
+// Row tiles of a chunk: 4, 6 or 8 (64-, 96- and 128-row chunks), or 2 up
+// to 32 rows, whichever the cost below rates cheapest.  Each chunk streams the weights again, and
 // a pass re-reads the chunk's activations, so wide chunks save weight bytes
 // while narrow ones leave registers for more column tiles a wave (fewer
 // passes): 192 rows run as two 96-row chunks in one pass each rather than a
 // 128-row chunk in two passes plus a 64-row one.
-static bool mr_rt_ok(int RT) { return RT == 4 || RT == 6 || RT == 8; }
+static bool mr_rt_ok(int RT) { return RT == 2 || RT == 4 || RT == 6 || RT == 8; }
 
 // Most column tiles one pass of a group holds (groups of ceil(U / n_cg)
 // units split into `passes` parts).
@@ -332,7 +333,7 @@ static long mr_max_pass_tiles(const MrPlan& m) {
 // accumulators 4 RT B, weight ring 8 B D and activation ring 2 D RT
 // registers a lane (ring depth D = 2 half K-blocks), within the 256 of a
 // wave at two waves per SIMD (checked: no spills).
-static int mr_max_cols(int RT) { return RT == 4 ? 4 : RT == 6 ? 3 : 2; }
+static int mr_max_cols(int RT) { return RT == 2 ? 6 : RT == 4 ? 4 : RT == 6 ? 3 : 2; }
 
 // Plan cost, in compute-unit clocks: a workgroup's requested bytes (its
 // weights, the activations of its K-range once per pass at half weight, as
@@ -355,17 +356,20 @@ static double mr_cost(const MrPlan& m, int cus) {
 }
 
 bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int max_splits) {
-  // Up to 32 rows the weight-streaming kernel is faster on every 7B-shaped
+  // Up to 24 rows the weight-streaming kernel is faster on every 7B-shaped
   // projection: both run at the weight stream's rate per compute unit, and
   // its many small workgroups balance the chip better than one workgroup
   // per compute unit with a whole number of column tiles (measured: gate/up
-  // 50.5 against 52.9 us, LM head 169 against 222 us at 16 rows).
-  if (R <= 32 || N % 16 || K % 128) return false;
+  // 50.5 against 52.9 us, LM head 169 against 222 us at 16 rows; steps at
+  // 17 / 20 / 24 rows +4.5 / +4.8 / +3.6% here).  From 25 rows its 2-row-tile
+  // blocks re-read as many activation bytes as weight bytes, and the column
+  // slices win (28 / 32 rows: -0.5 / -1.3%).
+  if (R <= 24 || N % 16 || K % 128) return false;
   const int gr = epi_kind == EPI_SWIGLU ? 2 : 1;
   if ((N / 16) % gr) return false;
   const int cus = std::max(1, n_cus);
   double best = -1;
-  for (int RT = 4; RT <= 8; RT += 2) {
+  for (int RT = R <= 32 ? 2 : 4; RT <= 8; RT += 2) {
     MrPlan t{};
     t.R = R;
     t.RT = RT;
@@ -441,7 +445,9 @@ static hipError_t launch_mr_b(const void* X, size_t xplane, const void* Wp, cons
     case 1: return launch_mr_t<RT, 1>(X, xplane, Wp, m, ep, st);
     case 2: return launch_mr_t<RT, 2>(X, xplane, Wp, m, ep, st);
     case 3: if constexpr (RT <= 6) return launch_mr_t<RT, 3>(X, xplane, Wp, m, ep, st); break;
-    case 4: if constexpr (RT == 4) return launch_mr_t<RT, 4>(X, xplane, Wp, m, ep, st); break;
+    case 4: if constexpr (RT <= 4) return launch_mr_t<RT, 4>(X, xplane, Wp, m, ep, st); break;
+    case 5: if constexpr (RT == 2) return launch_mr_t<RT, 5>(X, xplane, Wp, m, ep, st); break;
+    case 6: if constexpr (RT == 2) return launch_mr_t<RT, 6>(X, xplane, Wp, m, ep, st); break;
     default: break;
   }
   return hipErrorInvalidValue;
@@ -462,6 +468,7 @@ hipError_t launch_gemm_mr(const void* X, size_t xplane, const void* Wp, const Mr
   if (gemm_mr_lds_bytes(m) > 160 * 1024) return hipErrorInvalidValue;
   if (m.S > 1 && (!ep.kpart || (size_t)m.S * m.R * m.T * 16 > kGemmPartFloats)) return hipErrorInvalidValue;
   switch (m.RT) {
+    case 2: return launch_mr_b<2>(X, xplane, Wp, m, ep, st);
     case 4: return launch_mr_b<4>(X, xplane, Wp, m, ep, st);
     case 6: return launch_mr_b<6>(X, xplane, Wp, m, ep, st);
     case 8: return launch_mr_b<8>(X, xplane, Wp, m, ep, st);

@@ -108,7 +108,7 @@ size_t gemm_blocks(const GemmShape& s);
 // kernel reduces.
 struct MrPlan {
   int R;            // rows
-  int RT;           // row tiles per chunk (4, 6, 8): 16 RT rows per chunk
+  int RT;           // row tiles per chunk (2, 4, 6, 8): 16 RT rows per chunk
   int B;            // column tiles per wave at most
   int KC;           // 128-wide K-blocks
   int P;            // pack group of the weight matrix
