@@ -321,6 +321,22 @@ __global__ void __launch_bounds__(kRedThreads) k_mr_reduce(MrPlan m, Epi ep) {
 // 128-row chunk in two passes plus a 64-row one.
 static bool mr_rt_ok(int RT) { return RT == 2 || RT == 4 || RT == 6 || RT == 8; }
 
+// Row ranges where a measured chunk size beats the cost's choice (7B-shaped
+// steps after 1024 tokens, all projections at one row-tile count; us):
+// 128 rows 7382 (8) -> 7029 (4), 256 rows 11340 (8) -> 10774 (4), 224 rows
+// 10989 -> 10365 (4), 384 rows 14152 (8) -> 13937 (6).  The 64-row chunks
+// win where the rows fill 2 or 4 of them: the chunks of a column group run
+// on one XCD at the same time (their workgroup ids are congruent mod 8), so
+// their weight re-reads hit L2, which the cost charges as full requests,
+// while wider chunks re-read more activations per pass and load the matrix
+// cores more.  0: the cost decides.
+static int mr_measured_rt(int R) {
+  if (R > 96 && R <= 128) return 4;
+  if (R > 192 && R <= 256) return 4;
+  if (R > 320 && R <= 384) return 6;
+  return 0;
+}
+
 // Most column tiles one pass of a group holds (groups of ceil(U / n_cg)
 // units split into `passes` parts).
 static long mr_max_pass_tiles(const MrPlan& m) {
@@ -369,7 +385,9 @@ bool gemm_mr_plan(MrPlan& m, int R, int N, int K, int epi_kind, int n_cus, int m
   if ((N / 16) % gr) return false;
   const int cus = std::max(1, n_cus);
   double best = -1;
+  const int rt_fixed = mr_measured_rt(R);
   for (int RT = R <= 32 ? 2 : 4; RT <= 8; RT += 2) {
+    if (rt_fixed && RT != rt_fixed) continue;
     MrPlan t{};
     t.R = R;
     t.RT = RT;
