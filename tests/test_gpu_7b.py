@@ -112,10 +112,13 @@ def prompt1024():
     return jf_inputs.prompt(1, 1024, V)
 
 
-@pytest.mark.parametrize("n", [16, 64])
+@pytest.mark.parametrize("n", [16, 24, 64])
 def test_7b_step_window_logits(env, prompt1024, n):
-    """The benchmark's step (n = 16) and a two-chunk step (n = 64, the
-    projections run as two 32-row chunks): every row's logits and argmax."""
+    """The benchmark's step (n = 16: one row tile, gate/up with the tail
+    split), n = 24 (the weight-streaming kernel's two-row-tile blocks, gate/up
+    with the tail split) and n = 64 (the column-slice GEMM for gate/up, down
+    and the LM head, QKV and O as two 32-row chunks): every row's logits and
+    argmax."""
     import torch
     dec, model = env["dec"], env["model"]
     dec.reset()
