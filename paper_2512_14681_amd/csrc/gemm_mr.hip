@@ -314,11 +314,11 @@ __global__ void __launch_bounds__(kRedThreads) k_mr_reduce(MrPlan m, Epi ep) {
 
 // ---- plans ------------------------------------------------------------------------
 // Row tiles of a chunk: 4, 6 or 8 (64-, 96- and 128-row chunks), or 2 up
-// to 32 rows, whichever the cost below rates cheapest.  Each chunk streams the weights again, and
-// a pass re-reads the chunk's activations, so wide chunks save weight bytes
-// while narrow ones leave registers for more column tiles a wave (fewer
-// passes): 192 rows run as two 96-row chunks in one pass each rather than a
-// 128-row chunk in two passes plus a 64-row one.
+// to 32 rows, whichever the cost below rates cheapest.  Each chunk streams
+// the weights again, and a pass re-reads the chunk's activations, so wide
+// chunks save weight bytes while narrow ones leave registers for more
+// column tiles a wave (fewer passes): 192 rows run as two 96-row chunks in
+// one pass each rather than a 128-row chunk in two passes plus a 64-row one.
 static bool mr_rt_ok(int RT) { return RT == 2 || RT == 4 || RT == 6 || RT == 8; }
 
 // Row ranges where a measured chunk size beats the cost's choice (7B-shaped
