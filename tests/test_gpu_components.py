@@ -116,11 +116,12 @@ def test_lm_head_acceptance_closed_form():
     assert res[0] == R
 
 
-@pytest.mark.parametrize("R", [25, 32, 48, 80, 96, 128, 144, 192, 256])
+@pytest.mark.parametrize("R", [25, 32, 48, 80, 96, 128, 144, 192, 256, 384, 512])
 def test_lm_head_column_slice_chunks(R):
     """A vocabulary wide enough for the column-slice GEMM (2048 tiles of 16
-    columns, K = 1024): 32-, 64- and 96-row chunks, one to four of them
-    (128 and 256 rows: two and four 64-row chunks), with ragged last chunks
+    columns, K = 1024): 32-, 64-, 96- and 128-row chunks, one to four of
+    them (128 and 256 rows: two and four 64-row chunks; 384 rows: four
+    96-row chunks; 512 rows: four 128-row chunks), with ragged last chunks
     (25 = 32 - 7, 80 = 96 - 16, 144 = 96 + 48).  bf16 values, plain fp64
     product and argmax."""
     d, V = 1024, 32768
