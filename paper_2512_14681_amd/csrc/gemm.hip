@@ -1,5 +1,5 @@
 // Small-M weight-streaming GEMM for the decoder's projections:
-//   Y[R][N] = X[R][K] * W[N][K]^T,  R = rows of one Jacobi step (1..256).
+//   Y[R][N] = X[R][K] * W[N][K]^T,  R = rows of one Jacobi step (1..512).
 //
 // The step is bound by reading W once (Sec. 4.2 / App. D of the paper: the
 // extra draft rows of a Jacobi iteration are nearly free until the hardware

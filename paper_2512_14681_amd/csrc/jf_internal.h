@@ -171,7 +171,7 @@ struct AttnArgs {
   const int32_t* page_table;
   const int32_t* state;      // state[0] = C (device), or null: use C_host
   int C_host;
-  const uint64_t* vis;       // [R][4] or null (causal)
+  const uint64_t* vis;       // [R][kVisWords] or null (causal)
   float* o_part;             // [splits][R*H][hd]
   float* ml_part;            // [splits][R*H][2]
   void* out;                 // [R][H*hd] activation planes, GEMM-input layout
@@ -211,7 +211,7 @@ struct SideArgs {
   const float* rope_cos;
   const float* rope_sin;
   int32_t* flags;               // step flags (JF_FLAG_*)
-  const uint64_t* vis;          // [R][4] in-step visibility, or null (causal)
+  const uint64_t* vis;          // [R][kVisWords] in-step visibility, or null (causal)
   int keys_ub;                  // host bound of C + R: the key-split layout
   int qtiles, splits, split_keys;
   float* o_part;                // [splits][R * H][hd]
